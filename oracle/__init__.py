@@ -1,0 +1,23 @@
+"""CPU oracle of one rank's LAGA attention block — TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package. The product path (the HIP library and its
+Python binding) never calls it and shares no code with it.
+
+Modules:
+  * ``laga``     — the plain definition (explicit form), fp64 by default:
+                   reconstruct K/V, causal softmax attention, its backward.
+  * ``absorbed`` — the algebraically equivalent absorbed form (B2), used only
+                   as a pin of ``laga``; it materialises n_h*d_c intermediates,
+                   which is fine on the CPU and never happens on the GPU.
+
+Parity status: every function here is pinned by tests/test_oracle.py
+(brute force, absorbed form, finite differences, closed forms, invariants,
+causal prefix, torch SDPA). The paper prints no worked numeric example of the
+attention outputs, so no pin compares against values printed in the paper.
+"""
+from .laga import (reconstruct_kv, attn_fwd, attn_bwd, attn_fwd_rows,
+                   algorithmic_flops)
+
+__all__ = ["reconstruct_kv", "attn_fwd", "attn_bwd", "attn_fwd_rows",
+           "algorithmic_flops"]
