@@ -1,0 +1,149 @@
+/*
+ * laga.h — C ABI of one rank's share of LAGA (Latent All-Gather Attention).
+ *
+ * After the latent all-gather (Alg. 1 step 3) a rank holds, for the whole
+ * gathered sequence, the compressed latent c_kv [B,S,d_c] and the shared RoPE
+ * key k_pe [B,S,d_rope]; after the head-scatter (Alg. 1 step 2) it holds the
+ * queries q [B,S,H,d_nope+d_rope] of its H heads, and it owns the head shard
+ * W_kv_b [d_c, H*(d_nope+d_v)] of the up-projection. This library computes:
+ *
+ *   laga_reconstruct_kv : Alg. 1 step 4 — kv = c_kv @ W_kv_b (per-head K_nope, V)
+ *   laga_attn_fwd       : Alg. 1 step 5 — causal softmax attention with
+ *                         K_h = [K_nope,h || k_pe] (k_pe broadcast to all heads,
+ *                         property P2 of Section 2.1) and V_h; also returns the
+ *                         per-row log-sum-exp that the backward reuses
+ *   laga_attn_bwd       : the per-rank backward (Section 5.2 covers the
+ *                         collectives around it): dq, the head-shard partials
+ *                         dc_kv and dk_pe, and the W_kv_b shard gradient dW
+ *
+ * Layouts (all row-major, contiguous, device memory, 16-byte aligned):
+ *   c_kv   [B, S, d_c]                     element dtype
+ *   k_pe   [B, S, d_rope]                  element dtype
+ *   q      [B, S, H, d_nope + d_rope]      element dtype; q_nope first, then q_rope
+ *   w_kv_b [d_c, H * (d_nope + d_v)]       element dtype; head h owns the column
+ *                                          block [h*(d_nope+d_v), (h+1)*(d_nope+d_v)),
+ *                                          K_nope columns first, then V
+ *   kv     [B, S, H, d_nope + d_v]         element dtype (= [B*S, H*(d_nope+d_v)])
+ *   out    [B, S, H, d_v]                  element dtype
+ *   lse    [B, H, S]                       fp32, natural-log log-sum-exp of each row
+ *   dout   [B, S, H, d_v]                  element dtype
+ *   dq     [B, S, H, d_nope + d_rope]      element dtype
+ *   dc_kv  [B, S, d_c]                     element dtype (partial over this head shard)
+ *   dk_pe  [B, S, d_rope]                  element dtype (partial over this head shard)
+ *   dw_kv_b[d_c, H * (d_nope + d_v)]       fp32 (the full gradient of this shard)
+ *
+ * Conventions:
+ *   - Ownership: the caller owns every buffer, including the workspace; the
+ *     library allocates and frees nothing and keeps no state between calls.
+ *   - Asynchrony: work is enqueued on `stream` (a hipStream_t passed as void*,
+ *     NULL = the default stream); calls return without synchronising.
+ *   - Validation happens on the host before any launch; on error nothing is
+ *     launched and no output is touched. Asynchronous device faults surface at
+ *     the caller's next synchronisation. No exception crosses the ABI.
+ *   - Every output is overwritten, never accumulated into.
+ *   - Causal means key j is visible to query i iff j <= i (0-based positions in
+ *     the gathered sequence, S_q == S_k). Non-causal attends to every key.
+ *   - Supported head dims: (d_nope, d_rope, d_v) = (128, 64, 128) — DeepSeek-V3 —
+ *     and (32, 16, 32); d_c a multiple of 32 up to 1024; S >= 1; B >= 1; H >= 1.
+ *     Anything else returns LAGA_ERR_UNSUPPORTED.
+ *   - Results do not depend on H: every per-head output (kv columns, out, lse,
+ *     dq, dw_kv_b columns) of a head is bit-identical whichever head shard it is
+ *     computed in; with deterministic = 1 repeated calls are bit-identical.
+ */
+#ifndef LAGA_H_
+#define LAGA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define LAGA_API __attribute__((visibility("default")))
+#else
+#define LAGA_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LAGA_ABI_VERSION 1
+
+typedef enum {
+  LAGA_OK = 0,
+  LAGA_ERR_NULL = 1,        /* a required pointer (or the problem) is NULL */
+  LAGA_ERR_SHAPE = 2,       /* a dimension is <= 0 or sizes are inconsistent */
+  LAGA_ERR_UNSUPPORTED = 3, /* dims/dtype/mode this build has no kernel for */
+  LAGA_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+  LAGA_ERR_WORKSPACE = 5,   /* workspace smaller than laga_workspace_bytes() */
+  LAGA_ERR_DEVICE = 6       /* the HIP runtime reported an error at launch */
+} laga_status_t;
+
+typedef enum { LAGA_DTYPE_BF16 = 0, LAGA_DTYPE_FP32 = 1 } laga_dtype_t;
+
+/* Where attention gets its per-head K_nope/V from.
+ * MATERIALIZED: from `kv`, written beforehand by laga_reconstruct_kv.
+ * FUSED: rebuilt tile by tile on chip from c_kv and w_kv_b; no per-head K/V
+ *        tensor is ever written to HBM by the forward. */
+typedef enum { LAGA_KV_MATERIALIZED = 0, LAGA_KV_FUSED = 1 } laga_kv_mode_t;
+
+typedef enum { LAGA_OP_FWD = 0, LAGA_OP_BWD = 1 } laga_op_t;
+
+typedef struct {
+  int64_t batch;       /* B */
+  int64_t seq_len;     /* S: gathered sequence length */
+  int64_t n_heads;     /* H: heads of THIS rank's shard */
+  int64_t d_c;         /* latent width (d_kv) */
+  int64_t d_nope;      /* per-head no-RoPE q/k width */
+  int64_t d_rope;      /* shared RoPE band width */
+  int64_t d_v;         /* per-head value width */
+  float softmax_scale; /* multiplies q.k; the paper's 1/sqrt(d) with d = d_nope + d_rope */
+  int32_t causal;      /* 1: causal mask, 0: none */
+  int32_t dtype;       /* laga_dtype_t: element type of all non-fp32 tensors */
+  int32_t kv_mode;     /* laga_kv_mode_t */
+  int32_t deterministic; /* 1: no floating-point atomics; bitwise-reproducible */
+  int32_t reserved;    /* must be 0 */
+} laga_problem_t;
+
+/* Alg. 1 step 4: kv[b,t,:] = c_kv[b,t,:] @ w_kv_b, stored [B,S,H,d_nope+d_v].
+ * Accumulates in fp32 over d_c in ascending order; bf16 outputs are rounded to
+ * nearest-even. */
+LAGA_API laga_status_t laga_reconstruct_kv(const laga_problem_t* p, const void* c_kv,
+                                  const void* w_kv_b, void* kv, void* stream);
+
+/* Alg. 1 step 5 for the H heads of the shard: out and lse.
+ * kv is required (non-NULL) for MATERIALIZED and ignored for FUSED, which
+ * instead reads c_kv and w_kv_b. k_pe is shared by all heads. The workspace
+ * must hold laga_workspace_bytes(p, LAGA_OP_FWD) bytes (may be 0 / NULL). */
+LAGA_API laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q,
+                            const void* c_kv, const void* k_pe,
+                            const void* w_kv_b, const void* kv, void* out,
+                            float* lse, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* Backward of laga_reconstruct_kv + laga_attn_fwd given dout:
+ *   dq = dL/dq, dc_kv = dL/dc_kv and dk_pe = dL/dk_pe summed over this shard's
+ *   heads, dw_kv_b = dL/dW_kv_b (fp32, overwritten).
+ * out and lse are the forward's outputs. kv is required for MATERIALIZED; for
+ * FUSED it may be NULL and K/V are rebuilt into the workspace. */
+LAGA_API laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q,
+                            const void* c_kv, const void* k_pe,
+                            const void* w_kv_b, const void* kv, const void* out,
+                            const float* lse, const void* dout, void* dq,
+                            void* dc_kv, void* dk_pe, float* dw_kv_b,
+                            void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
+ * is invalid (check with the entry point itself for the error code). */
+LAGA_API size_t laga_workspace_bytes(const laga_problem_t* p, int op);
+
+/* Static, never-NULL description of a status code. */
+LAGA_API const char* laga_status_string(laga_status_t s);
+
+/* LAGA_ABI_VERSION of the built library. */
+LAGA_API int laga_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAGA_H_ */

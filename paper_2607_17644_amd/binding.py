@@ -1,0 +1,207 @@
+"""ctypes binding of include/laga.h (marshalling only; torch supplies memory and streams).
+
+Each ``laga_*`` function takes torch tensors, checks dtype/shape/device/
+contiguity, passes raw pointers and the current HIP stream to the C entry point
+of the same name, and raises :class:`LagaError` on a non-zero status. Outputs
+that are not supplied are allocated with torch (the C library never allocates).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_PKG, "liblaga.so")
+
+DTYPE_BF16, DTYPE_FP32 = 0, 1
+KV_MATERIALIZED, KV_FUSED = 0, 1
+OP_FWD, OP_BWD = 0, 1
+
+_STATUS = {0: "LAGA_OK", 1: "LAGA_ERR_NULL", 2: "LAGA_ERR_SHAPE", 3: "LAGA_ERR_UNSUPPORTED",
+           4: "LAGA_ERR_ALIGN", 5: "LAGA_ERR_WORKSPACE", 6: "LAGA_ERR_DEVICE"}
+
+
+class LagaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {laga_status_string(status)}")
+
+
+class _CProblem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seq_len", ctypes.c_int64), ("n_heads", ctypes.c_int64),
+                ("d_c", ctypes.c_int64), ("d_nope", ctypes.c_int64), ("d_rope", ctypes.c_int64),
+                ("d_v", ctypes.c_int64), ("softmax_scale", ctypes.c_float), ("causal", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("kv_mode", ctypes.c_int32), ("deterministic", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+@dataclasses.dataclass
+class Problem:
+    """Mirror of laga_problem_t."""
+    batch: int
+    seq_len: int
+    n_heads: int
+    d_c: int
+    d_nope: int
+    d_rope: int
+    d_v: int
+    softmax_scale: float | None = None  # default 1/sqrt(d_nope + d_rope)
+    causal: int = 1
+    dtype: int = DTYPE_BF16
+    kv_mode: int = KV_MATERIALIZED
+    deterministic: int = 1
+    reserved: int = 0
+
+    def c(self) -> _CProblem:
+        scale = self.softmax_scale
+        if scale is None:
+            scale = 1.0 / math.sqrt(self.d_nope + self.d_rope)
+        return _CProblem(self.batch, self.seq_len, self.n_heads, self.d_c, self.d_nope, self.d_rope,
+                         self.d_v, scale, self.causal, self.dtype, self.kv_mode, self.deterministic,
+                         self.reserved)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == DTYPE_BF16 else torch.float32
+
+    def shapes(self) -> dict:
+        B, S, H = self.batch, self.seq_len, self.n_heads
+        dqk, dkvh = self.d_nope + self.d_rope, self.d_nope + self.d_v
+        return {"c_kv": (B, S, self.d_c), "k_pe": (B, S, self.d_rope), "q": (B, S, H, dqk),
+                "w_kv_b": (self.d_c, H * dkvh), "kv": (B, S, H, dkvh), "out": (B, S, H, self.d_v),
+                "lse": (B, H, S), "dout": (B, S, H, self.d_v), "dq": (B, S, H, dqk),
+                "dc_kv": (B, S, self.d_c), "dk_pe": (B, S, self.d_rope), "dw_kv_b": (self.d_c, H * dkvh)}
+
+
+def _load():
+    if not os.path.exists(lib_path):
+        raise ImportError(f"{lib_path} is not built; run `python -m paper_2607_17644_amd.build`")
+    L = ctypes.CDLL(lib_path)
+    vp, P = ctypes.c_void_p, ctypes.POINTER(_CProblem)
+    L.laga_abi_version.restype = ctypes.c_int
+    L.laga_status_string.restype = ctypes.c_char_p
+    L.laga_status_string.argtypes = [ctypes.c_int]
+    L.laga_workspace_bytes.restype = ctypes.c_size_t
+    L.laga_workspace_bytes.argtypes = [P, ctypes.c_int]
+    L.laga_reconstruct_kv.restype = ctypes.c_int
+    L.laga_reconstruct_kv.argtypes = [P, vp, vp, vp, vp]
+    L.laga_attn_fwd.restype = ctypes.c_int
+    L.laga_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.laga_attn_bwd.restype = ctypes.c_int
+    L.laga_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    return L
+
+
+_lib = _load()
+
+
+def laga_abi_version() -> int:
+    return _lib.laga_abi_version()
+
+
+def laga_status_string(status: int) -> str:
+    return _lib.laga_status_string(status).decode()
+
+
+def laga_workspace_bytes(p: Problem, op: int) -> int:
+    return int(_lib.laga_workspace_bytes(ctypes.byref(p.c()), op))
+
+
+def _ptr(t, name, shape=None, dtype=None, required=True):
+    if t is None:
+        if required:
+            raise ValueError(f"{name} is required")
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(status, where):
+    if status != 0:
+        raise LagaError(status, where)
+
+
+def _new(p, name, dtype, device):
+    return torch.empty(p.shapes()[name], dtype=dtype, device=device)
+
+
+def laga_reconstruct_kv(p: Problem, c_kv, w_kv_b, kv=None, stream=None):
+    """kv = c_kv @ w_kv_b as [B,S,H,d_nope+d_v] (Alg. 1 step 4)."""
+    sh, dt = p.shapes(), p.torch_dtype
+    if kv is None:
+        kv = _new(p, "kv", dt, c_kv.device)
+    _check(_lib.laga_reconstruct_kv(ctypes.byref(p.c()), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
+                                    _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
+                                    _ptr(kv, "kv", sh["kv"], dt), _stream(stream)), "laga_reconstruct_kv")
+    return kv
+
+
+def _workspace(p, op, workspace, device):
+    need = laga_workspace_bytes(p, op)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return workspace
+
+
+def laga_attn_fwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv=None, out=None, lse=None, workspace=None,
+                  stream=None):
+    """Causal MLA attention forward of the shard's heads; returns (out, lse)."""
+    sh, dt = p.shapes(), p.torch_dtype
+    dev = q.device
+    if out is None:
+        out = _new(p, "out", dt, dev)
+    if lse is None:
+        lse = _new(p, "lse", torch.float32, dev)
+    workspace = _workspace(p, OP_FWD, workspace, dev)
+    _check(_lib.laga_attn_fwd(
+        ctypes.byref(p.c()), _ptr(q, "q", sh["q"], dt), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
+        _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
+        _ptr(kv, "kv", sh["kv"], dt, required=False), _ptr(out, "out", sh["out"], dt),
+        _ptr(lse, "lse", sh["lse"], torch.float32), _ptr(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)), "laga_attn_fwd")
+    return out, lse
+
+
+def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None, dc_kv=None,
+                  dk_pe=None, dw_kv_b=None, workspace=None, stream=None):
+    """Backward of the block; returns (dq, dc_kv, dk_pe, dw_kv_b)."""
+    sh, dt = p.shapes(), p.torch_dtype
+    dev = q.device
+    if dq is None:
+        dq = _new(p, "dq", dt, dev)
+    if dc_kv is None:
+        dc_kv = _new(p, "dc_kv", dt, dev)
+    if dk_pe is None:
+        dk_pe = _new(p, "dk_pe", dt, dev)
+    if dw_kv_b is None:
+        dw_kv_b = _new(p, "dw_kv_b", torch.float32, dev)
+    workspace = _workspace(p, OP_BWD, workspace, dev)
+    _check(_lib.laga_attn_bwd(
+        ctypes.byref(p.c()), _ptr(q, "q", sh["q"], dt), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
+        _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
+        _ptr(kv, "kv", sh["kv"], dt, required=False), _ptr(out, "out", sh["out"], dt),
+        _ptr(lse, "lse", sh["lse"], torch.float32), _ptr(dout, "dout", sh["dout"], dt),
+        _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], dt),
+        _ptr(dk_pe, "dk_pe", sh["dk_pe"], dt), _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
+        _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)),
+        "laga_attn_bwd")
+    return dq, dc_kv, dk_pe, dw_kv_b

@@ -1,0 +1,159 @@
+// C ABI of the per-rank LAGA attention block: validation, workspace layout and
+// dispatch to the gfx950 kernels. Declarations and conventions: include/laga.h.
+#include <math.h>
+#include <stdint.h>
+
+#include "laga.h"
+#include "kernels.hpp"
+
+using namespace laga;
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;  // 32-bit element offsets inside kernels
+
+struct Dims {
+  int B, S, H, d_c, dn, dr, dv;
+  int dqk() const { return dn + dr; }
+  int dkvh() const { return dn + dv; }
+};
+
+bool is_v3(const laga_problem_t* p) { return p->d_nope == 128 && p->d_rope == 64 && p->d_v == 128; }
+bool is_small(const laga_problem_t* p) { return p->d_nope == 32 && p->d_rope == 16 && p->d_v == 32; }
+
+laga_status_t validate(const laga_problem_t* p, Dims* d) {
+  if (!p) return LAGA_ERR_NULL;
+  if (p->batch <= 0 || p->seq_len <= 0 || p->n_heads <= 0 || p->d_c <= 0 || p->d_nope <= 0 ||
+      p->d_rope <= 0 || p->d_v <= 0)
+    return LAGA_ERR_SHAPE;
+  if (!isfinite(p->softmax_scale) || !(p->softmax_scale > 0.f)) return LAGA_ERR_SHAPE;
+  if ((p->causal != 0 && p->causal != 1) || (p->deterministic != 0 && p->deterministic != 1) ||
+      p->reserved != 0)
+    return LAGA_ERR_UNSUPPORTED;
+  if (p->dtype != LAGA_DTYPE_BF16 && p->dtype != LAGA_DTYPE_FP32) return LAGA_ERR_UNSUPPORTED;
+  if (p->kv_mode != LAGA_KV_MATERIALIZED && p->kv_mode != LAGA_KV_FUSED) return LAGA_ERR_UNSUPPORTED;
+  if (!is_v3(p) && !is_small(p)) return LAGA_ERR_UNSUPPORTED;
+  if (p->d_c % 32 != 0 || p->d_c > 1024) return LAGA_ERR_UNSUPPORTED;
+  const int64_t tok = p->batch * p->seq_len;
+  const int64_t wide = p->n_heads * (p->d_nope + (p->d_rope > p->d_v ? p->d_rope : p->d_v) +
+                                     (p->d_nope > p->d_v ? p->d_nope : p->d_v));
+  if (tok >= kMaxElems || tok * wide >= kMaxElems || tok * p->d_c >= kMaxElems ||
+      p->d_c * p->n_heads * (p->d_nope + p->d_v) * 16 >= kMaxElems)
+    return LAGA_ERR_UNSUPPORTED;
+  d->B = (int)p->batch; d->S = (int)p->seq_len; d->H = (int)p->n_heads; d->d_c = (int)p->d_c;
+  d->dn = (int)p->d_nope; d->dr = (int)p->d_rope; d->dv = (int)p->d_v;
+  return LAGA_OK;
+}
+
+bool misaligned(const void* ptr) { return ((uintptr_t)ptr & 15u) != 0; }
+
+size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ? 2 : 4; }
+
+size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Backward workspace: [delta | dKV | dK_pe per head | dW split partials | kv rebuild]
+struct BwdWs {
+  size_t delta, dkv, dkpe_h, dw_part, kv, total;
+};
+BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
+  BwdWs w{};
+  const size_t tok = (size_t)d.B * d.S;
+  size_t off = 0;
+  w.delta = off; off += round_up(sizeof(float) * tok * d.H);
+  w.dkv = off; off += round_up(elem_size(p) * tok * d.H * d.dkvh());
+  w.dkpe_h = off; off += round_up(sizeof(float) * tok * d.H * d.dr);
+  const size_t ns = dw_split_count((int)tok);
+  w.dw_part = off; off += ns > 1 ? round_up(sizeof(float) * ns * d.d_c * d.H * d.dkvh()) : 0;
+  w.kv = off; off += p->kv_mode == LAGA_KV_FUSED ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
+  w.total = off;
+  return w;
+}
+
+size_t fwd_ws_bytes(const laga_problem_t* p, const Dims& d) {
+  (void)p; (void)d;
+  return 0;
+}
+
+laga_status_t from_hip(hipError_t e) { return e == hipSuccess ? LAGA_OK : LAGA_ERR_DEVICE; }
+
+template <typename T>
+laga_status_t reconstruct_t(const Dims& d, const void* c, const void* w, void* kv, hipStream_t st) {
+  return from_hip(launch_reconstruct<T>((const T*)c, (const T*)w, (T*)kv, d.B * d.S, d.H * d.dkvh(), d.d_c, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+int laga_abi_version(void) { return LAGA_ABI_VERSION; }
+
+const char* laga_status_string(laga_status_t s) {
+  switch (s) {
+    case LAGA_OK: return "LAGA_OK: success";
+    case LAGA_ERR_NULL: return "LAGA_ERR_NULL: a required pointer is NULL";
+    case LAGA_ERR_SHAPE: return "LAGA_ERR_SHAPE: a dimension is not positive or the scale is not finite and positive";
+    case LAGA_ERR_UNSUPPORTED: return "LAGA_ERR_UNSUPPORTED: head dims, d_c, dtype, mode or size not supported by this build";
+    case LAGA_ERR_ALIGN: return "LAGA_ERR_ALIGN: a pointer is not 16-byte aligned";
+    case LAGA_ERR_WORKSPACE: return "LAGA_ERR_WORKSPACE: workspace smaller than laga_workspace_bytes()";
+    case LAGA_ERR_DEVICE: return "LAGA_ERR_DEVICE: the HIP runtime reported a launch error";
+  }
+  return "unknown laga_status_t";
+}
+
+size_t laga_workspace_bytes(const laga_problem_t* p, int op) {
+  Dims d;
+  if (validate(p, &d) != LAGA_OK) return 0;
+  if (op == LAGA_OP_FWD) return fwd_ws_bytes(p, d);
+  if (op == LAGA_OP_BWD) return bwd_layout(p, d).total;
+  return 0;
+}
+
+laga_status_t laga_reconstruct_kv(const laga_problem_t* p, const void* c_kv, const void* w_kv_b, void* kv,
+                                  void* stream) {
+  Dims d;
+  laga_status_t s = validate(p, &d);
+  if (s != LAGA_OK) return s;
+  if (!c_kv || !w_kv_b || !kv) return LAGA_ERR_NULL;
+  if (misaligned(c_kv) || misaligned(w_kv_b) || misaligned(kv)) return LAGA_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  return p->dtype == LAGA_DTYPE_BF16 ? reconstruct_t<bf16>(d, c_kv, w_kv_b, kv, st)
+                                     : reconstruct_t<float>(d, c_kv, w_kv_b, kv, st);
+}
+
+laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
+                            const void* w_kv_b, const void* kv, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  Dims d;
+  laga_status_t s = validate(p, &d);
+  if (s != LAGA_OK) return s;
+  const bool fused = p->kv_mode == LAGA_KV_FUSED;
+  if (!q || !c_kv || !k_pe || !w_kv_b || !out || !lse || (!fused && !kv)) return LAGA_ERR_NULL;
+  if (misaligned(q) || misaligned(c_kv) || misaligned(k_pe) || misaligned(w_kv_b) || misaligned(out) ||
+      misaligned(lse) || (!fused && misaligned(kv)))
+    return LAGA_ERR_ALIGN;
+  const size_t need = fwd_ws_bytes(p, d);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return LAGA_ERR_WORKSPACE;
+  if (need > 0 && misaligned(workspace)) return LAGA_ERR_ALIGN;
+  if (fused) return LAGA_ERR_UNSUPPORTED;
+  AttnFwdArgs a{};
+  a.q = q; a.k_pe = k_pe; a.kv = kv; a.c_kv = c_kv; a.w_t = nullptr; a.out = out; a.lse = lse;
+  a.B = d.B; a.S = d.S; a.H = d.H; a.d_c = d.d_c; a.scale = p->softmax_scale; a.causal = p->causal;
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf = p->dtype == LAGA_DTYPE_BF16;
+  if (is_v3(p)) return from_hip(bf ? launch_attn_fwd<bf16, 128, 64, 128>(a, st) : launch_attn_fwd<float, 128, 64, 128>(a, st));
+  return from_hip(bf ? launch_attn_fwd<bf16, 32, 16, 32>(a, st) : launch_attn_fwd<float, 32, 16, 32>(a, st));
+}
+
+laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
+                            const void* w_kv_b, const void* kv, const void* out, const float* lse,
+                            const void* dout, void* dq, void* dc_kv, void* dk_pe, float* dw_kv_b,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  laga_status_t s = validate(p, &d);
+  if (s != LAGA_OK) return s;
+  (void)q; (void)c_kv; (void)k_pe; (void)w_kv_b; (void)kv; (void)out; (void)lse; (void)dout; (void)dq;
+  (void)dc_kv; (void)dk_pe; (void)dw_kv_b; (void)workspace; (void)workspace_bytes; (void)stream;
+  return LAGA_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// Host-side launchers of the gfx950 kernels (all enqueue on the given stream).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include "common.hpp"
+
+namespace laga {
+
+// Tokens per split of the dW reduction (fixed: never depends on the head count).
+constexpr int kDwSplitTokens = 2048;
+size_t dw_split_count(int tokens);
+
+template <typename T>
+hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st);
+template <typename T>
+hipError_t launch_dc(const T* dkv, const T* w, T* dc, int M, int N, int K, hipStream_t st);
+template <typename T>
+hipError_t launch_dw(const T* c, const T* dkv, float* dw, float* partial, int M, int N, int K, hipStream_t st);
+
+struct AttnFwdArgs {
+  const void* q;      // [B,S,H,DN+DR]
+  const void* k_pe;   // [B,S,DR]
+  const void* kv;     // [B,S,H,DN+DV] (materialised path)
+  const void* c_kv;   // [B,S,d_c]     (fused path)
+  const void* w_t;    // [H*(DN+DV), d_c] transposed W_kv_b (fused path)
+  void* out;          // [B,S,H,DV]
+  float* lse;         // [B,H,S]
+  int B, S, H, d_c;
+  float scale;
+  int causal;
+};
+
+template <typename T, int DN, int DR, int DV>
+hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
+
+struct AttnBwdArgs {
+  const void* q;
+  const void* k_pe;
+  const void* kv;    // [B,S,H,DN+DV]
+  const void* out;
+  const void* dout;
+  const float* lse;
+  void* dq;          // [B,S,H,DN+DR]
+  void* dk_pe;       // [B,S,DR]
+  float* delta;      // workspace [B,H,S]
+  void* dkv;         // workspace [B,S,H,DN+DV]
+  float* dkpe_h;     // workspace [B,S,H,DR]
+  int B, S, H;
+  float scale;
+  int causal;
+};
+
+// delta, dK/dV (into dkv, dkpe_h), dQ and the dk_pe head sum; dc_kv / dW are the GEMMs above.
+template <typename T, int DN, int DR, int DV>
+hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t st);
+
+}  // namespace laga

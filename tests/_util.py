@@ -1,0 +1,40 @@
+"""Shared test helpers: device tensors from the seeded inputs, error metrics."""
+import math
+
+import numpy as np
+
+import laga_inputs as LI
+
+
+def problem_for(w, **kw):
+    import paper_2607_17644_amd as L
+    return L.Problem(batch=w.batch, seq_len=w.seq_len, n_heads=w.n_heads, d_c=w.d_c,
+                     d_nope=w.d_nope, d_rope=w.d_rope, d_v=w.d_v, softmax_scale=w.scale,
+                     causal=int(w.causal), dtype=L.DTYPE_BF16 if w.dtype == "bf16" else L.DTYPE_FP32,
+                     **kw)
+
+
+def to_dev(x, dtype_name):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    t = t.to(torch.bfloat16 if dtype_name == "bf16" else torch.float32)
+    return t.cuda()
+
+
+def dev_inputs(w, x):
+    return {k: to_dev(v, w.dtype) for k, v in x.items()}
+
+
+def f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def err(gpu, ref):
+    """max |gpu - ref| / max(1, rms(ref)): raw max-abs for unit-scale tensors,
+    scaled for sums over many terms (dW over tokens, dc_kv over columns)."""
+    d = np.max(np.abs(gpu - ref)) if ref.size else 0.0
+    rms = math.sqrt(float(np.mean(ref * ref))) if ref.size else 0.0
+    return d / max(1.0, rms)
+
+
+TOL = {"bf16": 2e-2, "fp32": 1e-4}

@@ -1,0 +1,81 @@
+"""The C ABI: library loads, exports what include/laga.h declares, and rejects
+invalid arguments on the host before any launch (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "laga.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"LAGA_API\s+[\w\s\*]+?\b(laga_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    syms = declared_symbols()
+    for s in ("laga_reconstruct_kv", "laga_attn_fwd", "laga_attn_bwd", "laga_workspace_bytes",
+              "laga_status_string", "laga_abi_version"):
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2607_17644_amd as L
+    lib = ctypes.CDLL(L.lib_path)
+    for s in declared_symbols():
+        assert hasattr(lib, s), s
+
+
+def test_version_and_status_strings():
+    import paper_2607_17644_amd as L
+    assert L.laga_abi_version() == 1
+    for code in range(7):
+        assert L.laga_status_string(code).startswith("LAGA_")
+    assert "unknown" in L.laga_status_string(99)
+
+
+def _raw():
+    import paper_2607_17644_amd.binding as B
+    return B._lib, B
+
+
+def test_validation_errors_without_launch():
+    lib, B = _raw()
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    fake = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
+    vp = ctypes.c_void_p
+    # NULL problem
+    assert lib.laga_reconstruct_kv(None, fake, fake, fake, None) == 1
+    # NULL tensor
+    assert lib.laga_reconstruct_kv(ctypes.byref(P.c()), None, fake, fake, None) == 1
+    # bad shape
+    for field, val in (("seq_len", 0), ("n_heads", -1), ("d_c", 0), ("softmax_scale", float("nan"))):
+        Q = B.Problem(**{**P.__dict__, field: val})
+        assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 2, field
+    # unsupported
+    for field, val in (("d_nope", 64), ("d_c", 48), ("d_c", 2048), ("dtype", 7), ("kv_mode", 3),
+                       ("causal", 2), ("deterministic", 5), ("reserved", 1)):
+        Q = B.Problem(**{**P.__dict__, field: val})
+        assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 3, field
+    # misaligned
+    assert lib.laga_reconstruct_kv(ctypes.byref(P.c()), vp(0x10008), fake, fake, None) == 4
+    # workspace sizes: forward needs none in materialised mode, backward some
+    assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 1) > 0
+    assert lib.laga_workspace_bytes(None, 0) == 0
+
+
+def test_attention_entry_points_validate_first():
+    lib, B = _raw()
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    fake = ctypes.c_void_p(0x10000)
+    z = None
+    # materialised forward without kv -> NULL
+    assert lib.laga_attn_fwd(ctypes.byref(P.c()), fake, fake, fake, fake, z, fake, fake, z, 0, z) == 1
+    # backward with too little workspace
+    need = lib.laga_workspace_bytes(ctypes.byref(P.c()), 1)
+    st = lib.laga_attn_bwd(ctypes.byref(P.c()), fake, fake, fake, fake, fake, fake, fake, fake,
+                           fake, fake, fake, fake, fake, need - 1, z)
+    assert st == 5

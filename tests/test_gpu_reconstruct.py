@@ -1,0 +1,63 @@
+"""laga_reconstruct_kv (Alg. 1 step 4) against the oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import laga_inputs as LI
+from oracle import laga as O
+from _util import TOL, dev_inputs, err, f64, problem_for
+
+pytestmark = pytest.mark.gpu
+
+
+def run(w):
+    import paper_2607_17644_amd as L
+    x = LI.make_inputs(w, with_dout=False)
+    d = dev_inputs(w, x)
+    kv = L.laga_reconstruct_kv(problem_for(w), d["c_kv"], d["w_kv_b"])
+    ref = O.reconstruct_kv(x["c_kv"], x["w_kv_b"], w.n_heads, w.d_nope, w.d_v)
+    return f64(kv), ref, x, d
+
+
+@pytest.mark.parametrize("name,S", [("tiny_fp32", 256), ("tiny_fp32", 7), ("tiny_fp32", 300)])
+def test_fp32(name, S):
+    w = LI.WORKLOADS[name].replace(seq_len=S)
+    got, ref, _, _ = run(w)
+    assert err(got, ref) < TOL["fp32"]
+
+
+@pytest.mark.parametrize("S,H", [(4096, 16), (1, 16), (333, 3), (129, 1)])
+def test_bf16(S, H):
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=S, n_heads=H)
+    got, ref, _, _ = run(w)
+    assert err(got, ref) < TOL["bf16"]
+    # the fp32 accumulation is rounded once to bf16: within one bf16 ulp of the exact
+    # value, plus the fp32 accumulation error (absolute, ~1e-7 per unit term) near zero
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+    assert np.all(np.abs(got - ref) <= ulp + 1e-5)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_head_slices_bitwise(dtype):
+    """kv columns of a 16-head shard are bit-identical to the same columns of the 128-head run."""
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_full_h128_s4096"].replace(seq_len=520, dtype=dtype)
+    x = LI.make_inputs(w, with_dout=False)
+    d = dev_inputs(w, x)
+    full = L.laga_reconstruct_kv(problem_for(w), d["c_kv"], d["w_kv_b"])
+    ws = w.replace(n_heads=16)
+    for r in range(8):
+        wcols = d["w_kv_b"][:, r * 16 * 256:(r + 1) * 16 * 256].contiguous()
+        part = L.laga_reconstruct_kv(problem_for(ws), d["c_kv"], wcols)
+        assert torch.equal(part, full[:, :, r * 16:(r + 1) * 16]), r
+
+
+def test_repeatable():
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=1000)
+    x = LI.make_inputs(w, with_dout=False)
+    d = dev_inputs(w, x)
+    a = L.laga_reconstruct_kv(problem_for(w), d["c_kv"], d["w_kv_b"])
+    b = L.laga_reconstruct_kv(problem_for(w), d["c_kv"], d["w_kv_b"])
+    assert torch.equal(a, b)
