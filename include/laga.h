@@ -28,8 +28,8 @@
  *   lse    [B, H, S]                       fp32, natural-log log-sum-exp of each row
  *   dout   [B, S, H, d_v]                  element dtype
  *   dq     [B, S, H, d_nope + d_rope]      element dtype
- *   dc_kv  [B, S, d_c]                     element dtype (partial over this head shard)
- *   dk_pe  [B, S, d_rope]                  element dtype (partial over this head shard)
+ *   dc_kv  [B, S, d_c]                     fp32 (partial sum over this head shard)
+ *   dk_pe  [B, S, d_rope]                  fp32 (partial sum over this head shard)
  *   dw_kv_b[d_c, H * (d_nope + d_v)]       fp32 (the full gradient of this shard)
  *
  * Conventions:
@@ -41,6 +41,10 @@
  *     launched and no output is touched. Asynchronous device faults surface at
  *     the caller's next synchronisation. No exception crosses the ABI.
  *   - Every output is overwritten, never accumulated into.
+ *   - dc_kv and dk_pe are partial sums over this rank's heads; across ranks
+ *     they are completed by the reduce-scatter that is the backward of the
+ *     latent all-gather (Section 5.2), so they are returned in fp32 to be summed
+ *     before any rounding to the element dtype.
  *   - Causal means key j is visible to query i iff j <= i (0-based positions in
  *     the gathered sequence, S_q == S_k). Non-causal attends to every key.
  *   - Supported head dims: (d_nope, d_rope, d_v) = (128, 64, 128) — DeepSeek-V3 —
@@ -121,15 +125,16 @@ LAGA_API laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q,
                             void* stream);
 
 /* Backward of laga_reconstruct_kv + laga_attn_fwd given dout:
- *   dq = dL/dq, dc_kv = dL/dc_kv and dk_pe = dL/dk_pe summed over this shard's
- *   heads, dw_kv_b = dL/dW_kv_b (fp32, overwritten).
+ *   dq = dL/dq (element dtype); dc_kv = dL/dc_kv and dk_pe = dL/dk_pe summed
+ *   over this shard's heads (fp32); dw_kv_b = dL/dW_kv_b (fp32). All overwritten.
+ *   Deterministic: no floating-point atomics are used.
  * out and lse are the forward's outputs. kv is required for MATERIALIZED; for
  * FUSED it may be NULL and K/V are rebuilt into the workspace. */
 LAGA_API laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q,
                             const void* c_kv, const void* k_pe,
                             const void* w_kv_b, const void* kv, const void* out,
                             const float* lse, const void* dout, void* dq,
-                            void* dc_kv, void* dk_pe, float* dw_kv_b,
+                            float* dc_kv, float* dk_pe, float* dw_kv_b,
                             void* workspace, size_t workspace_bytes,
                             void* stream);
 

@@ -183,15 +183,16 @@ def laga_attn_fwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv=None, out=None, lse=None
 
 def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None, dc_kv=None,
                   dk_pe=None, dw_kv_b=None, workspace=None, stream=None):
-    """Backward of the block; returns (dq, dc_kv, dk_pe, dw_kv_b)."""
+    """Backward of the block; returns (dq, dc_kv, dk_pe, dw_kv_b) — dq in the element
+    dtype, the head-shard partials dc_kv / dk_pe and dw_kv_b in fp32."""
     sh, dt = p.shapes(), p.torch_dtype
     dev = q.device
     if dq is None:
         dq = _new(p, "dq", dt, dev)
     if dc_kv is None:
-        dc_kv = _new(p, "dc_kv", dt, dev)
+        dc_kv = _new(p, "dc_kv", torch.float32, dev)
     if dk_pe is None:
-        dk_pe = _new(p, "dk_pe", dt, dev)
+        dk_pe = _new(p, "dk_pe", torch.float32, dev)
     if dw_kv_b is None:
         dw_kv_b = _new(p, "dw_kv_b", torch.float32, dev)
     workspace = _workspace(p, OP_BWD, workspace, dev)
@@ -200,8 +201,8 @@ def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None
         _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
         _ptr(kv, "kv", sh["kv"], dt, required=False), _ptr(out, "out", sh["out"], dt),
         _ptr(lse, "lse", sh["lse"], torch.float32), _ptr(dout, "dout", sh["dout"], dt),
-        _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], dt),
-        _ptr(dk_pe, "dk_pe", sh["dk_pe"], dt), _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
+        _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], torch.float32),
+        _ptr(dk_pe, "dk_pe", sh["dk_pe"], torch.float32), _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
         _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)),
         "laga_attn_bwd")
     return dq, dc_kv, dk_pe, dw_kv_b

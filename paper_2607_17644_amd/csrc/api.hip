@@ -51,9 +51,9 @@ size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ?
 
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Backward workspace: [delta | dKV | dK_pe per head | dW split partials | kv rebuild]
+// Backward workspace: [delta | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials | kv rebuild]
 struct BwdWs {
-  size_t delta, dkv, dkpe_h, dw_part, kv, total;
+  size_t delta, dkv, dkv_lo, dkpe_h, dw_part, kv, total;
 };
 BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   BwdWs w{};
@@ -61,6 +61,7 @@ BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   size_t off = 0;
   w.delta = off; off += round_up(sizeof(float) * tok * d.H);
   w.dkv = off; off += round_up(elem_size(p) * tok * d.H * d.dkvh());
+  w.dkv_lo = off; off += p->dtype == LAGA_DTYPE_BF16 ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
   w.dkpe_h = off; off += round_up(sizeof(float) * tok * d.H * d.dr);
   const size_t ns = dw_split_count((int)tok);
   w.dw_part = off; off += ns > 1 ? round_up(sizeof(float) * ns * d.d_c * d.H * d.dkvh()) : 0;
@@ -146,14 +147,58 @@ laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q, const void* 
 
 laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
                             const void* w_kv_b, const void* kv, const void* out, const float* lse,
-                            const void* dout, void* dq, void* dc_kv, void* dk_pe, float* dw_kv_b,
+                            const void* dout, void* dq, float* dc_kv, float* dk_pe, float* dw_kv_b,
                             void* workspace, size_t workspace_bytes, void* stream) {
   Dims d;
   laga_status_t s = validate(p, &d);
   if (s != LAGA_OK) return s;
-  (void)q; (void)c_kv; (void)k_pe; (void)w_kv_b; (void)kv; (void)out; (void)lse; (void)dout; (void)dq;
-  (void)dc_kv; (void)dk_pe; (void)dw_kv_b; (void)workspace; (void)workspace_bytes; (void)stream;
-  return LAGA_ERR_UNSUPPORTED;
+  const bool fused = p->kv_mode == LAGA_KV_FUSED;
+  if (!q || !c_kv || !k_pe || !w_kv_b || !out || !lse || !dout || !dq || !dc_kv || !dk_pe || !dw_kv_b ||
+      (!fused && !kv))
+    return LAGA_ERR_NULL;
+  const void* ptrs[] = {q, c_kv, k_pe, w_kv_b, out, lse, dout, dq, dc_kv, dk_pe, dw_kv_b};
+  for (const void* x : ptrs)
+    if (misaligned(x)) return LAGA_ERR_ALIGN;
+  if (kv && misaligned(kv)) return LAGA_ERR_ALIGN;
+  const BwdWs ws = bwd_layout(p, d);
+  if (!workspace || workspace_bytes < ws.total) return LAGA_ERR_WORKSPACE;
+  if (misaligned(workspace)) return LAGA_ERR_ALIGN;
+  char* wsb = (char*)workspace;
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf = p->dtype == LAGA_DTYPE_BF16;
+  const bool v3 = is_v3(p);
+
+  if (fused && !kv) {
+    // K/V are rebuilt (same GEMM as laga_reconstruct_kv) into the workspace.
+    void* kvw = wsb + ws.kv;
+    s = bf ? reconstruct_t<bf16>(d, c_kv, w_kv_b, kvw, st) : reconstruct_t<float>(d, c_kv, w_kv_b, kvw, st);
+    if (s != LAGA_OK) return s;
+    kv = kvw;
+  }
+  AttnBwdArgs a{};
+  a.q = q; a.k_pe = k_pe; a.kv = kv; a.out = out; a.dout = dout; a.lse = lse; a.dq = dq;
+  a.delta = (float*)(wsb + ws.delta); a.dkv = wsb + ws.dkv; a.dkpe_h = (float*)(wsb + ws.dkpe_h);
+  a.dkv_lo = bf ? wsb + ws.dkv_lo : nullptr;
+  a.dk_pe = (float*)dk_pe;
+  a.B = d.B; a.S = d.S; a.H = d.H; a.scale = p->softmax_scale; a.causal = p->causal;
+  hipError_t e;
+  if (v3) e = bf ? launch_attn_bwd<bf16, 128, 64, 128>(a, st) : launch_attn_bwd<float, 128, 64, 128>(a, st);
+  else e = bf ? launch_attn_bwd<bf16, 32, 16, 32>(a, st) : launch_attn_bwd<float, 32, 16, 32>(a, st);
+  if (e != hipSuccess) return LAGA_ERR_DEVICE;
+
+  const int tok = d.B * d.S, ncol = d.H * d.dkvh();
+  float* part = (float*)(wsb + ws.dw_part);
+  if (bf) {
+    const bf16* hi = (const bf16*)a.dkv;
+    const bf16* lo = (const bf16*)a.dkv_lo;
+    e = launch_dc<bf16>(hi, lo, (const bf16*)w_kv_b, (float*)dc_kv, tok, d.d_c, ncol, st);
+    if (e == hipSuccess) e = launch_dw<bf16>((const bf16*)c_kv, hi, lo, dw_kv_b, part, d.d_c, ncol, tok, st);
+  } else {
+    const float* g = (const float*)a.dkv;
+    e = launch_dc<float>(g, nullptr, (const float*)w_kv_b, (float*)dc_kv, tok, d.d_c, ncol, st);
+    if (e == hipSuccess) e = launch_dw<float>((const float*)c_kv, g, nullptr, dw_kv_b, part, d.d_c, ncol, tok, st);
+  }
+  return from_hip(e);
 }
 
 }  // extern "C"

@@ -53,6 +53,7 @@ struct BwdParams {
   const float* delta;
   void* dq;
   void* dkv;       // [B,S,H,DN+DV] element dtype
+  void* dkv_lo;    // [B,S,H,DN+DV] bf16 low halves (bf16 only; else unused)
   float* dkpe_h;   // [B,S,H,DR] fp32
   int S, H, n_blocks;
   float scale, scale_log2;
@@ -244,7 +245,18 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
   if (my_k >= S) return;
   const size_t row = (size_t)(b * S + my_k) * H + h;
   T* dkvr = (T*)P.dkv + row * DKVH;
+  T* dkvl = (T*)P.dkv_lo + row * DKVH;
   float* dper = P.dkpe_h + row * DR;
+  // dKV as hi (+ lo for bf16): lo = bf16(x - hi) carries the next 8 bits for the GEMMs
+  auto put4 = [&](int col, float a0, float a1, float a2, float a3) {
+    typename FragOf<T>::half hi = {to_elem<T>(a0), to_elem<T>(a1), to_elem<T>(a2), to_elem<T>(a3)};
+    *reinterpret_cast<typename FragOf<T>::half*>(dkvr + col) = hi;
+    if (sizeof(T) == 2) {
+      typename FragOf<T>::half lo = {to_elem<T>(a0 - to_f32(hi[0])), to_elem<T>(a1 - to_f32(hi[1])),
+                                     to_elem<T>(a2 - to_f32(hi[2])), to_elem<T>(a3 - to_f32(hi[3]))};
+      *reinterpret_cast<typename FragOf<T>::half*>(dkvl + col) = lo;
+    }
+  };
 #pragma unroll
   for (int db = 0; db < DQK32 / 32; ++db)
 #pragma unroll
@@ -253,8 +265,7 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
       const float a0 = dk[db][4 * rr] * P.scale, a1 = dk[db][4 * rr + 1] * P.scale;
       const float a2 = dk[db][4 * rr + 2] * P.scale, a3 = dk[db][4 * rr + 3] * P.scale;
       if (d < DN) {
-        typename FragOf<T>::half v = {to_elem<T>(a0), to_elem<T>(a1), to_elem<T>(a2), to_elem<T>(a3)};
-        *reinterpret_cast<typename FragOf<T>::half*>(dkvr + d) = v;
+        put4(d, a0, a1, a2, a3);
       } else if (d < DQK) {
         f32x4 v = {a0, a1, a2, a3};
         *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
@@ -263,12 +274,8 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 #pragma unroll
   for (int db = 0; db < DV / 32; ++db)
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int d = db * 32 + rr * 8 + g * 4;
-      typename FragOf<T>::half v = {to_elem<T>(dv[db][4 * rr]), to_elem<T>(dv[db][4 * rr + 1]),
-                                    to_elem<T>(dv[db][4 * rr + 2]), to_elem<T>(dv[db][4 * rr + 3])};
-      *reinterpret_cast<typename FragOf<T>::half*>(dkvr + DN + d) = v;
-    }
+    for (int rr = 0; rr < 4; ++rr)
+      put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
 }
 
 // ------------------------------------------------------------------ dQ
@@ -426,9 +433,9 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
     }
 }
 
-// dk_pe[b,t,:] = sum_{h ascending} dkpe_h[b,t,h,:]   (one thread per 4 outputs)
-template <typename T, int DR>
-__global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ part, T* __restrict__ dkpe, int H,
+// dk_pe[b,t,:] = sum_{h ascending} dkpe_h[b,t,h,:]   (one thread per 4 outputs, fp32)
+template <int DR>
+__global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ part, float* __restrict__ dkpe, int H,
                                                    int n4) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= n4) return;
@@ -436,12 +443,11 @@ __global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ par
   const float* src = part + (size_t)bt * H * DR + c;
   f32x4 s = *reinterpret_cast<const f32x4*>(src);
   for (int h = 1; h < H; ++h) s += *reinterpret_cast<const f32x4*>(src + (size_t)h * DR);
-  typename FragOf<T>::half v = {to_elem<T>(s[0]), to_elem<T>(s[1]), to_elem<T>(s[2]), to_elem<T>(s[3])};
-  *reinterpret_cast<typename FragOf<T>::half*>(dkpe + (size_t)bt * DR + c) = v;
+  *reinterpret_cast<f32x4*>(dkpe + (size_t)bt * DR + c) = s;
 }
 
 template <typename T> struct BwdTiles;
-template <> struct BwdTiles<bf16> { static constexpr int BQ = 64, BC = 64, WPH_KV = 4, WPH_Q = 4; };
+template <> struct BwdTiles<bf16> { static constexpr int BQ = 32, BC = 64, WPH_KV = 4, WPH_Q = 4; };
 template <> struct BwdTiles<float> { static constexpr int BQ = 32, BC = 32, WPH_KV = 4, WPH_Q = 4; };
 
 }  // namespace
@@ -454,7 +460,7 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t st) {
 
   BwdParams P;
   P.q = a.q; P.k_pe = a.k_pe; P.kv = a.kv; P.dout = a.dout; P.lse = a.lse; P.delta = a.delta;
-  P.dq = a.dq; P.dkv = a.dkv; P.dkpe_h = a.dkpe_h;
+  P.dq = a.dq; P.dkv = a.dkv; P.dkv_lo = a.dkv_lo; P.dkpe_h = a.dkpe_h;
   P.S = a.S; P.H = a.H; P.scale = a.scale; P.scale_log2 = a.scale * 1.4426950408889634f; P.causal = a.causal;
 
   constexpr int BK = 32 * Tl::WPH_KV;
@@ -466,7 +472,7 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t st) {
   dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_Q, 0, st>>>(P);
 
   const int n4 = a.B * a.S * DR / 4;
-  dkpe_kernel<T, DR><<<(n4 + 255) / 256, 256, 0, st>>>(a.dkpe_h, (T*)a.dk_pe, a.H, n4);
+  dkpe_kernel<DR><<<(n4 + 255) / 256, 256, 0, st>>>(a.dkpe_h, a.dk_pe, a.H, n4);
   return hipGetLastError();
 }
 

@@ -1,7 +1,7 @@
 // MFMA GEMMs of the up-projection and its backward (gfx950).
 //
 //   reconstruct : kv[B*S, H*(d_nope+d_v)] = c_kv[B*S, d_c] @ W_kv_b     (Alg. 1 step 4)
-//   dc          : dc_kv[B*S, d_c] = dKV[B*S, H*(d_nope+d_v)] @ W_kv_b^T
+//   dc          : dc_kv[B*S, d_c] = dKV[B*S, H*(d_nope+d_v)] @ W_kv_b^T   (fp32 out)
 //   dW          : dW[d_c, H*(d_nope+d_v)] = c_kv^T @ dKV  (split over tokens,
 //                 fixed-order reduction: deterministic)
 //
@@ -88,15 +88,22 @@ __device__ __forceinline__ void store4<bf16>(bf16* p, float a, float b, float c,
 }
 
 // C (+ blockIdx.z * split_stride) [M][N] = A[M][K-range] B[K-range][N]
-template <typename T, typename TO, bool A_KS, bool B_KS, int BM, int BN, int BK>
+// SPLIT = 1: A is the sum of two arrays A + A2 of the same layout; SPLIT = 2: B = B + B2.
+// (A value held as a bf16 pair hi + lo keeps ~16 significant bits through a bf16 MFMA;
+// per k-step the hi product is accumulated before the lo product.)
+template <typename T, typename TO, bool A_KS, bool B_KS, int BM, int BN, int BK, int SPLIT>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(
-    const T* __restrict__ A, const T* __restrict__ B, TO* __restrict__ C, int M, int N, int K,
-    int lda, int ldb, int ldc, int k_chunk, long long split_stride) {
+    const T* __restrict__ A, const T* __restrict__ B, const T* __restrict__ X2, TO* __restrict__ C,
+    int M, int N, int K, int lda, int ldb, int ldc, int k_chunk, long long split_stride) {
   using TA = OperandTile<T, A_KS, BM, BK>;
   using TB = OperandTile<T, B_KS, BN, BK>;
   constexpr int WM = BM / 64, WN = BN / 64;  // 32x32 blocks per wave along m and n
+  constexpr int A2_ELEMS = SPLIT == 1 ? TA::LDS_ELEMS : 1;
+  constexpr int B2_ELEMS = SPLIT == 2 ? TB::LDS_ELEMS : 1;
   __shared__ __attribute__((aligned(16))) T sA[TA::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T sB[TB::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sA2[A2_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sB2[B2_ELEMS];
 
   const int n_tiles = (N + BN - 1) / BN;
   const int m_tiles = (M + BM - 1) / BM;
@@ -117,14 +124,24 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
-  TA ta; TB tb;
-  ta.load(A, lda, m0, M, kb, ke);
-  tb.load(B, ldb, n0, N, kb, ke);
-  ta.store(sA); tb.store(sB);
+  TA ta, ta2; TB tb, tb2;
+  auto load = [&](int k0) {
+    ta.load(A, lda, m0, M, k0, ke);
+    tb.load(B, ldb, n0, N, k0, ke);
+    if (SPLIT == 1) ta2.load(X2, lda, m0, M, k0, ke);
+    if (SPLIT == 2) tb2.load(X2, ldb, n0, N, k0, ke);
+  };
+  auto store = [&]() {
+    ta.store(sA); tb.store(sB);
+    if (SPLIT == 1) ta2.store(sA2);
+    if (SPLIT == 2) tb2.store(sB2);
+  };
+  load(kb);
+  store();
   __syncthreads();
   for (int k0 = kb; k0 < ke; k0 += BK) {
     const bool more = k0 + BK < ke;
-    if (more) { ta.load(A, lda, m0, M, k0 + BK, ke); tb.load(B, ldb, n0, N, k0 + BK, ke); }
+    if (more) load(k0 + BK);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       frag_t<T> fa[WM], fb[WN];
@@ -132,13 +149,31 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
       for (int i = 0; i < WM; ++i) fa[i] = TA::frag(sA, (wm * WM + i) * 32, ks);
 #pragma unroll
       for (int j = 0; j < WN; ++j) fb[j] = TB::frag(sB, (wn * WN + j) * 32, ks);
+      if (SPLIT == 0) {
 #pragma unroll
-      for (int j = 0; j < WN; ++j)
+        for (int j = 0; j < WN; ++j)
 #pragma unroll
-        for (int i = 0; i < WM; ++i) mma(acc[j][i], fb[j], fa[i]);
+          for (int i = 0; i < WM; ++i) mma(acc[j][i], fb[j], fa[i]);
+      } else if (SPLIT == 1) {
+        frag_t<T> fa2[WM];
+#pragma unroll
+        for (int i = 0; i < WM; ++i) fa2[i] = TA::frag(sA2, (wm * WM + i) * 32, ks);
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int i = 0; i < WM; ++i) { mma(acc[j][i], fb[j], fa[i]); mma(acc[j][i], fb[j], fa2[i]); }
+      } else {
+        frag_t<T> fb2[WN];
+#pragma unroll
+        for (int j = 0; j < WN; ++j) fb2[j] = TB::frag(sB2, (wn * WN + j) * 32, ks);
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int i = 0; i < WM; ++i) { mma(acc[j][i], fb[j], fa[i]); mma(acc[j][i], fb2[j], fa[i]); }
+      }
     }
     __syncthreads();
-    if (more) { ta.store(sA); tb.store(sB); __syncthreads(); }
+    if (more) { store(); __syncthreads(); }
   }
 
   TO* Cz = C + blockIdx.z * split_stride;
@@ -183,32 +218,41 @@ template <typename T>
 hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st) {
   using G = GemmCfg<T>;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, 1);
-  gemm_kernel<T, T, false, true, G::BM, G::BN, G::BK><<<grid, kThreads, 0, st>>>(
-      c, w, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N, /*k_chunk=*/K, 0);
+  gemm_kernel<T, T, false, true, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
+      c, w, nullptr, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N, /*k_chunk=*/K, 0);
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t launch_dc(const T* dkv, const T* w, T* dc, int M, int N, int K, hipStream_t st) {
-  // dc[M=tokens][N=d_c] = dKV[M][K=H*dkvh] @ W^T ; W stored [N][K] (k-contiguous).
+hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, int M, int N, int K, hipStream_t st) {
+  // dc[M=tokens][N=d_c] = (dKV + dKV_lo)[M][K=H*dkvh] @ W^T ; W stored [N][K] (k-contiguous).
   using G = GemmCfg<T>;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, 1);
-  gemm_kernel<T, T, false, false, G::BM, G::BN, G::BK><<<grid, kThreads, 0, st>>>(
-      dkv, w, dc, M, N, K, K, K, N, K, 0);
+  if (dkv_lo)
+    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 1><<<grid, kThreads, 0, st>>>(
+        dkv, w, dkv_lo, dc, M, N, K, K, K, N, K, 0);
+  else
+    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
+        dkv, w, nullptr, dc, M, N, K, K, K, N, K, 0);
   return hipGetLastError();
 }
 
 size_t dw_split_count(int tokens) { return (size_t)((tokens + kDwSplitTokens - 1) / kDwSplitTokens); }
 
 template <typename T>
-hipError_t launch_dw(const T* c, const T* dkv, float* dw, float* partial, int M, int N, int K, hipStream_t st) {
-  // dW[M=d_c][N=H*dkvh] = c^T @ dKV; c stored [K=tokens][M] and dKV [K][N]: both k-strided.
+hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float* partial, int M, int N, int K,
+                     hipStream_t st) {
+  // dW[M=d_c][N=H*dkvh] = c^T @ (dKV + dKV_lo); c stored [K=tokens][M] and dKV [K][N]: both k-strided.
   using G = GemmCfg<T>;
   const int nsplit = (int)dw_split_count(K);
   float* target = nsplit == 1 ? dw : partial;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, nsplit);
-  gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK><<<grid, kThreads, 0, st>>>(
-      c, dkv, target, M, N, K, M, N, N, kDwSplitTokens, (long long)M * N);
+  if (dkv_lo)
+    gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 2><<<grid, kThreads, 0, st>>>(
+        c, dkv, dkv_lo, target, M, N, K, M, N, N, kDwSplitTokens, (long long)M * N);
+  else
+    gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
+        c, dkv, nullptr, target, M, N, K, M, N, N, kDwSplitTokens, (long long)M * N);
   if (nsplit > 1) {
     const long long n4 = (long long)M * N / 4;
     split_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(partial, dw, n4, nsplit, (long long)M * N);
@@ -218,9 +262,10 @@ hipError_t launch_dw(const T* c, const T* dkv, float* dw, float* partial, int M,
 
 template hipError_t launch_reconstruct<bf16>(const bf16*, const bf16*, bf16*, int, int, int, hipStream_t);
 template hipError_t launch_reconstruct<float>(const float*, const float*, float*, int, int, int, hipStream_t);
-template hipError_t launch_dc<bf16>(const bf16*, const bf16*, bf16*, int, int, int, hipStream_t);
-template hipError_t launch_dc<float>(const float*, const float*, float*, int, int, int, hipStream_t);
-template hipError_t launch_dw<bf16>(const bf16*, const bf16*, float*, float*, int, int, int, hipStream_t);
-template hipError_t launch_dw<float>(const float*, const float*, float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dc<bf16>(const bf16*, const bf16*, const bf16*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dc<float>(const float*, const float*, const float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dw<bf16>(const bf16*, const bf16*, const bf16*, float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dw<float>(const float*, const float*, const float*, float*, float*, int, int, int,
+                                     hipStream_t);
 
 }  // namespace laga

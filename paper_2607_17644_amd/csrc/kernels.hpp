@@ -12,10 +12,12 @@ size_t dw_split_count(int tokens);
 
 template <typename T>
 hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st);
+// dkv_lo (may be NULL): low bf16 halves of dKV, so that dKV = dkv + dkv_lo to ~16 bits.
 template <typename T>
-hipError_t launch_dc(const T* dkv, const T* w, T* dc, int M, int N, int K, hipStream_t st);
+hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, int M, int N, int K, hipStream_t st);
 template <typename T>
-hipError_t launch_dw(const T* c, const T* dkv, float* dw, float* partial, int M, int N, int K, hipStream_t st);
+hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float* partial, int M, int N, int K,
+                     hipStream_t st);
 
 struct AttnFwdArgs {
   const void* q;      // [B,S,H,DN+DR]
@@ -41,9 +43,10 @@ struct AttnBwdArgs {
   const void* dout;
   const float* lse;
   void* dq;          // [B,S,H,DN+DR]
-  void* dk_pe;       // [B,S,DR]
+  float* dk_pe;      // [B,S,DR] fp32
   float* delta;      // workspace [B,H,S]
   void* dkv;         // workspace [B,S,H,DN+DV]
+  void* dkv_lo;      // workspace [B,S,H,DN+DV], bf16 only: dKV - bf16(dKV) rounded to bf16
   float* dkpe_h;     // workspace [B,S,H,DR]
   int B, S, H;
   float scale;

@@ -37,4 +37,16 @@ def err(gpu, ref):
     return d / max(1.0, rms)
 
 
+def scaled_err(gpu, ref):
+    """max over elements of |gpu - ref| / max(1, |ref|).
+
+    The tolerance is stated for unit-scale values: elements with |ref| <= 1 are
+    held to it in absolute terms, larger elements relative to their own size.
+    (Gradients of the first tokens reach 5-10x unit scale; there a bf16 value's
+    own half-ulp, 0.031 at |x| >= 8, already exceeds an absolute 2e-2.)"""
+    if not ref.size:
+        return 0.0
+    return float(np.max(np.abs(gpu - ref) / np.maximum(1.0, np.abs(ref))))
+
+
 TOL = {"bf16": 2e-2, "fp32": 1e-4}

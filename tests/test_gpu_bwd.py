@@ -1,0 +1,136 @@
+"""laga_attn_bwd against the oracle, through the C ABI: dq, dc_kv, dk_pe, dW_kv_b."""
+import numpy as np
+import pytest
+
+import laga_inputs as LI
+from oracle import laga as O
+from _util import TOL, dev_inputs, err, f64, problem_for, scaled_err
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ("dq", "dc_kv", "dk_pe", "dw_kv_b")
+
+
+# dk_pe sums the rope-band gradient of every head; at the first keys it is the small
+# difference of larger per-head terms. A CPU emulation of exactly this path's bf16 rounding
+# points (bf16 K/V, P and dZ as MFMA operands, bf16 out in delta) lands at 1.9-2.2e-2 on it,
+# i.e. the 2e-2 bar is this tensor's bf16 noise floor; it is held to 1.5x that bar.
+DKPE_BF16_TOL = 3e-2
+
+
+def tol_for(name, dtype):
+    return DKPE_BF16_TOL if (name == "dk_pe" and dtype == "bf16") else TOL[dtype]
+
+
+def metric(name):
+    """Token-local tensors are held element-wise to tol * max(1, |ref|); dW, a sum over
+    all tokens, is held to tol * max(1, rms(dW))."""
+    return err if name == "dw_kv_b" else scaled_err
+
+
+def gpu_step(w, d, **kw):
+    import paper_2607_17644_amd as L
+    p = problem_for(w, **kw)
+    kv = L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"])
+    out, lse = L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv)
+    g = L.laga_attn_bwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"])
+    return dict(zip(NAMES, g)), out, lse
+
+
+def okw(w):
+    return dict(n_heads=w.n_heads, d_nope=w.d_nope, d_v=w.d_v, scale=w.scale, causal=w.causal)
+
+
+def check_full(w):
+    x = LI.make_inputs(w)
+    g, _, _ = gpu_step(w, dev_inputs(w, x))
+    ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+    errs = {k: metric(k)(f64(g[k]), ref[k]) for k in NAMES}
+    rms_errs = {k: err(f64(g[k]), ref[k]) for k in NAMES}
+    print(f"{w.name} S={w.seq_len} H={w.n_heads} B={w.batch} causal={w.causal}: " +
+          " ".join(f"{k} {v:.2e} (rms-scaled {rms_errs[k]:.2e})" for k, v in errs.items()))
+    for k, v in errs.items():
+        assert v < tol_for(k, w.dtype), (k, v)
+
+
+@pytest.mark.parametrize("S,B,causal", [(256, 1, True), (1, 1, True), (7, 2, True), (100, 1, True),
+                                        (257, 2, True), (256, 1, False), (45, 2, False)])
+def test_tiny_fp32(S, B, causal):
+    check_full(LI.WORKLOADS["tiny_fp32"].replace(seq_len=S, batch=B, causal=causal))
+
+
+@pytest.mark.parametrize("S,H,B,causal", [(2048, 16, 1, True), (1, 1, 1, True), (7, 3, 2, True),
+                                          (257, 3, 2, True), (300, 2, 1, False)])
+def test_v3_bf16(S, H, B, causal):
+    check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal))
+
+
+def test_v3_fp32_mode():
+    check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=300, n_heads=2, dtype="fp32"))
+
+
+def test_s16384_sampled():
+    """Training step at the per-rank shard (S=16384, 16 heads), as the benchmark runs it.
+    dq on sampled rows (row by row); dKV-derived rows dc_kv / dk_pe on the last keys, which
+    only see the last queries; dW through <W, dW> = <c_kv, dc_kv>; invariants."""
+    w = LI.WORKLOADS["v3_train_s16384"]
+    x = LI.make_inputs(w)
+    g, out, _ = gpu_step(w, dev_inputs(w, x))
+    rows = [0, 1, 100, 5000, 16383]
+    r = O.attn_fwd_rows(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], rows, dout=x["dout"],
+                        n_heads=16, d_nope=128, d_v=128, scale=w.scale)
+    assert scaled_err(f64(g["dq"][:, rows]), r["dq"]) < TOL["bf16"]
+    tail = w.seq_len - 128
+    rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
+    for k in ("dq", "dc_kv", "dk_pe"):
+        e = scaled_err(f64(g[k][:, tail:]), rb[k][:, tail:])
+        print(f"S=16384 tail rows {k}: {e:.3e}")
+        assert e < tol_for(k, "bf16"), (k, e)
+    check_invariants(x, g)
+
+
+def check_invariants(x, g):
+    """Exact identities (P6) evaluated on the GPU's gradients, at bf16-level tolerance."""
+    dk_pe, dc, dw = f64(g["dk_pe"]), f64(g["dc_kv"]), f64(g["dw_kv_b"])
+    c = x["c_kv"].astype(np.float64); W = x["w_kv_b"].astype(np.float64)
+    S = c.shape[1]
+    # sum over keys of dk_pe vanishes (softmax shift invariance)
+    assert np.max(np.abs(dk_pe.sum(axis=1))) < 2e-2 * np.sqrt(S) * max(1.0, np.sqrt(np.mean(dk_pe ** 2)))
+    a, b = np.sum(W * dw), np.sum(c * dc)
+    assert abs(a - b) < 1e-2 * max(1.0, abs(a), np.sqrt(np.sum(dc ** 2)))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_head_partition_bitwise(dtype):
+    """Per-head gradients (dq, dW columns) of two 8-head shards are bit-identical to the
+    16-head run; the head-summed partials dc_kv and dk_pe add up to the full ones."""
+    import torch
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=520 if dtype == "fp32" else 2048, dtype=dtype)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    full, _, _ = gpu_step(w, d)
+    ws = w.replace(n_heads=8)
+    acc_dc = 0; acc_dkpe = 0
+    for r in range(2):
+        hs = slice(r * 8, (r + 1) * 8)
+        ds = {"q": d["q"][:, :, hs].contiguous(), "c_kv": d["c_kv"], "k_pe": d["k_pe"],
+              "w_kv_b": d["w_kv_b"][:, r * 2048:(r + 1) * 2048].contiguous(),
+              "dout": d["dout"][:, :, hs].contiguous()}
+        g, _, _ = gpu_step(ws, ds)
+        assert torch.equal(g["dq"], full["dq"][:, :, hs]), r
+        assert torch.equal(g["dw_kv_b"], full["dw_kv_b"][:, r * 2048:(r + 1) * 2048]), r
+        acc_dc = acc_dc + f64(g["dc_kv"]); acc_dkpe = acc_dkpe + f64(g["dk_pe"])
+    # fp32 partials: the host-side sum differs from the full run only by summation order
+    assert scaled_err(acc_dc, f64(full["dc_kv"])) < 1e-4
+    assert scaled_err(acc_dkpe, f64(full["dk_pe"])) < 1e-4
+
+
+def test_repeatable():
+    import torch
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=700, n_heads=3)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    a, _, _ = gpu_step(w, d)
+    b, _, _ = gpu_step(w, d)
+    for k in NAMES:
+        assert torch.equal(a[k], b[k]), k
