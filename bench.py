@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Benchmark of one rank's LAGA attention block on one MI355X.
+
+One step = laga_reconstruct_kv + laga_attn_fwd + laga_attn_bwd (materialised K/V)
+on the per-rank training workload: DeepSeek-V3 shard of SP=8 (16 heads, d_c=512,
+q/k width 192, v width 128), S=16384, batch 1, bf16, seeded synthetic inputs
+already resident in HBM. Prints ONE JSON line (see --help).
+
+Metric: algorithmic TFLOP/s of the step (causal pairs counted as S^2/2;
+attention fwd 320*S^2*H, bwd 640*S^2*H, up-projection 3 x 2*S*d_c*H*256),
+ms per step, and the fraction of the MI355X dense bf16 MFMA peak.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD = "v3_train_s16384"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seq-len", type=int, default=None, help="override S (sweep); default 16384")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=8,
+                    help="heads of the workload the CPU oracle runs as its bounded sample")
+    ap.add_argument("--fused-compare", action="store_true",
+                    help="also time the forward with K/V rebuilt on chip (kv_mode=FUSED)")
+    return ap.parse_args()
+
+
+def flops(w):
+    from oracle.laga import algorithmic_flops  # pure arithmetic helper, no oracle compute
+    return algorithmic_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
+
+
+def gpu_bench(w, steps, warmup, fused_compare):
+    import torch
+    import laga_inputs as LI
+    import paper_2607_17644_amd as L
+
+    x = LI.make_inputs(w)
+    dev = torch.device("cuda:0")
+    d = {k: torch.from_numpy(v).to(torch.bfloat16).to(dev) for k, v in x.items()}
+    p = L.Problem(batch=w.batch, seq_len=w.seq_len, n_heads=w.n_heads, d_c=w.d_c, d_nope=w.d_nope,
+                  d_rope=w.d_rope, d_v=w.d_v, softmax_scale=w.scale, causal=1, dtype=L.DTYPE_BF16,
+                  kv_mode=L.KV_MATERIALIZED, deterministic=1)
+    sh = p.shapes()
+    bf, f32 = torch.bfloat16, torch.float32
+    kv = torch.empty(sh["kv"], dtype=bf, device=dev)
+    out = torch.empty(sh["out"], dtype=bf, device=dev)
+    lse = torch.empty(sh["lse"], dtype=f32, device=dev)
+    dq = torch.empty(sh["dq"], dtype=bf, device=dev)
+    dc = torch.empty(sh["dc_kv"], dtype=f32, device=dev)
+    dkpe = torch.empty(sh["dk_pe"], dtype=f32, device=dev)
+    dw = torch.empty(sh["dw_kv_b"], dtype=f32, device=dev)
+    ws_f = torch.empty(max(1, L.laga_workspace_bytes(p, L.OP_FWD)), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(1, L.laga_workspace_bytes(p, L.OP_BWD)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # the backward runs as its four stages (exactly what laga_attn_bwd does) so that each
+    # stage's kernels can be timed with events on the stream they are launched on
+    stages = [("bwd_prepare", L.BWD_PREPARE), ("bwd_dkdv", L.BWD_DKDV), ("bwd_dq", L.BWD_DQ),
+              ("bwd_finish", L.BWD_FINISH)]
+    names = ["reconstruct_kv", "attn_fwd"] + [n for n, _ in stages]
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"], kv=kv, stream=stream)
+        if ev: ev[1].record(stream)
+        L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv, out=out, lse=lse,
+                        workspace=ws_f, stream=stream)
+        if ev: ev[2].record(stream)
+        for i, (_, st) in enumerate(stages):
+            L.laga_attn_bwd_stage(st, p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"],
+                                  dq, dc, dkpe, dw, ws_b, stream=stream)
+            if ev: ev[3 + i].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    parts = {n: [] for n in names + ["attn_bwd", "step"]}
+    for e in evs:
+        for i, n in enumerate(names):
+            parts[n].append(e[i].elapsed_time(e[i + 1]))
+        parts["attn_bwd"].append(e[2].elapsed_time(e[len(names)]))
+        parts["step"].append(e[0].elapsed_time(e[len(names)]))
+    res = {"wall_ms_per_step": 1e3 * wall / steps,
+           "ms": {k: sum(v) / len(v) for k, v in parts.items()},
+           "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
+    assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
+
+    if fused_compare:
+        pf = L.Problem(**{**p.__dict__, "kv_mode": L.KV_FUSED})
+        ws_ff = torch.empty(max(1, L.laga_workspace_bytes(pf, L.OP_FWD)), dtype=torch.uint8, device=dev)
+        out_f = torch.empty_like(out); lse_f = torch.empty_like(lse)
+        fe = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        try:
+            for i in range(warmup + steps):
+                if i == warmup: fe[0].record(stream)
+                L.laga_attn_fwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], out=out_f, lse=lse_f,
+                                workspace=ws_ff, stream=stream)
+            fe[1].record(stream)
+            torch.cuda.synchronize()
+            res["fused_fwd_ms"] = fe[0].elapsed_time(fe[1]) / steps
+            res["fused_vs_materialised_max_abs"] = float((out_f.float() - out.float()).abs().max())
+        except L.LagaError as e:
+            res["fused_fwd_ms"] = None
+            res["fused_error"] = str(e)
+    return res
+
+
+def cpu_baseline(w, heads):
+    """The oracle as it stands (numpy fp64), on `heads` heads of the same workload."""
+    import numpy as np
+    import laga_inputs as LI
+    from oracle import laga as O
+    from oracle.laga import algorithmic_flops
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
+    except Exception:
+        threads = os.cpu_count()
+    ws = w.replace(n_heads=heads)
+    x = {k: v.astype(np.float64) for k, v in LI.make_inputs(ws).items()}
+    kw = dict(n_heads=heads, d_nope=ws.d_nope, d_v=ws.d_v, scale=ws.scale)
+    t0 = time.perf_counter()
+    O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **kw)
+    O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **kw)
+    dt = time.perf_counter() - t0
+    f = algorithmic_flops(ws.batch, ws.seq_len, heads, ws.d_c, ws.d_qk, ws.d_v, ws.d_kvh)
+    return {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"oracle fp64 numpy fwd+bwd (bwd recomputes the forward) of {heads} of {w.n_heads} "
+                      f"heads at S={w.seq_len}: {f / 1e9:.1f} GFLOP in {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the per-rank block has no "
+                          "inter-GPU step (the collectives around it are out of scope); "
+                          "run with --gpus 1"}))
+        sys.exit(2)
+    import laga_inputs as LI
+    w = LI.WORKLOADS[WORKLOAD]
+    if a.seq_len:
+        w = w.replace(seq_len=a.seq_len)
+    fl = flops(w)
+    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare)
+    ms = g["ms"]["step"]
+    tflops = fl / (ms * 1e-3) / 1e12
+
+    # roofline of the dominant kernel, the key-stationary backward (one launch per
+    # BWD_DKDV stage): algorithmic flops = the dV, dP and dK products, 2*(d_v + d_v + d_qk)
+    # = 896 flops per causal (query, key) pair and head, over S^2/2 pairs x H heads
+    S, H = w.seq_len, w.n_heads
+    pairs = float(w.batch) * S * S / 2 * H
+    dkdv_flops = pairs * 2 * (2 * w.d_v + w.d_qk)
+    achieved = dkdv_flops / (g["ms"]["bwd_dkdv"] * 1e-3) / 1e12
+    roofline = {"kernel": "dkdv_kernel", "bound": "mfma", "achieved": round(achieved, 1),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "avg_launch_ms": round(g["ms"]["bwd_dkdv"], 4),
+                "algorithmic_gflop_per_launch": round(dkdv_flops / 1e9, 1)}
+    fwd_flops = 2 * pairs * (w.d_qk + w.d_v)
+    other = {"attn_fwd_kernel": round(fwd_flops / (g["ms"]["attn_fwd"] * 1e-3) / 1e12, 1),
+             "dq_kernel_dQ_only": round(pairs * 2 * w.d_qk / (g["ms"]["bwd_dq"] * 1e-3) / 1e12, 1)}
+    cpu = None
+    if not a.no_cpu_baseline:
+        cpu = cpu_baseline(w, a.cpu_heads)
+    line = {
+        "metric": "attention-block TFLOP/s and ms/step (fwd+bwd), S=16384, 16 heads, % bf16 MFMA peak",
+        "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms, 4), "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; DeepSeek-V3 per-rank shapes)",
+        "config": {"workload": w.name if not a.seq_len else f"{w.name}@S={w.seq_len}", "seq_len": S,
+                   "n_heads": H, "d_c": w.d_c, "d_nope": w.d_nope, "d_rope": w.d_rope, "d_v": w.d_v,
+                   "batch": w.batch, "causal": True, "kv_mode": "materialised", "deterministic": True,
+                   "algorithmic_gflop_per_step": round(fl / 1e9, 1)},
+        "ms_breakdown": {k: round(v, 4) for k, v in g["ms"].items()},
+        "ms_min_max_step": [round(g["ms_min_step"], 4), round(g["ms_max_step"], 4)],
+        "roofline": roofline,
+        "algorithmic_tflops_by_kernel": other,
+        "cpu_baseline": cpu,
+    }
+    if a.fused_compare:
+        line["fused_fwd_ms"] = g.get("fused_fwd_ms")
+        if "fused_error" in g:
+            line["fused_error"] = g["fused_error"]
+        if "fused_vs_materialised_max_abs" in g:
+            line["fused_vs_materialised_max_abs"] = g["fused_vs_materialised_max_abs"]
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -138,6 +138,31 @@ LAGA_API laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q,
                             void* workspace, size_t workspace_bytes,
                             void* stream);
 
+/* The backward in its stages; laga_attn_bwd runs all four in this order on one
+ * stream. A caller may run them itself (same arguments and workspace for every
+ * stage) to put other work between them or to time them one by one:
+ *   LAGA_BWD_PREPARE  per-row delta = sum(dout * out) (and the K/V rebuild of
+ *                     the FUSED mode when kv is NULL)
+ *   LAGA_BWD_DKDV     key-stationary attention backward: dK, dV of every key
+ *   LAGA_BWD_DQ       query-stationary attention backward: dq
+ *   LAGA_BWD_FINISH   dk_pe head sum, dc_kv and dw_kv_b up-projection GEMMs
+ * Each stage reads what the previous ones left in the workspace. */
+typedef enum {
+  LAGA_BWD_PREPARE = 0,
+  LAGA_BWD_DKDV = 1,
+  LAGA_BWD_DQ = 2,
+  LAGA_BWD_FINISH = 3
+} laga_bwd_stage_t;
+
+LAGA_API laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p,
+                                           const void* q, const void* c_kv,
+                                           const void* k_pe, const void* w_kv_b,
+                                           const void* kv, const void* out,
+                                           const float* lse, const void* dout,
+                                           void* dq, float* dc_kv, float* dk_pe,
+                                           float* dw_kv_b, void* workspace,
+                                           size_t workspace_bytes, void* stream);
+
 /* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
  * is invalid (check with the entry point itself for the error code). */
 LAGA_API size_t laga_workspace_bytes(const laga_problem_t* p, int op);

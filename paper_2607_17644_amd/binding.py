@@ -20,6 +20,7 @@ lib_path = os.path.join(_PKG, "liblaga.so")
 DTYPE_BF16, DTYPE_FP32 = 0, 1
 KV_MATERIALIZED, KV_FUSED = 0, 1
 OP_FWD, OP_BWD = 0, 1
+BWD_PREPARE, BWD_DKDV, BWD_DQ, BWD_FINISH = 0, 1, 2, 3
 
 _STATUS = {0: "LAGA_OK", 1: "LAGA_ERR_NULL", 2: "LAGA_ERR_SHAPE", 3: "LAGA_ERR_UNSUPPORTED",
            4: "LAGA_ERR_ALIGN", 5: "LAGA_ERR_WORKSPACE", 6: "LAGA_ERR_DEVICE"}
@@ -79,7 +80,7 @@ class Problem:
 
 def _load():
     if not os.path.exists(lib_path):
-        raise ImportError(f"{lib_path} is not built; run `python -m paper_2607_17644_amd.build`")
+        raise ImportError(f"{lib_path} is not built; run `python paper_2607_17644_amd/build.py`")
     L = ctypes.CDLL(lib_path)
     vp, P = ctypes.c_void_p, ctypes.POINTER(_CProblem)
     L.laga_abi_version.restype = ctypes.c_int
@@ -93,6 +94,9 @@ def _load():
     L.laga_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.laga_attn_bwd.restype = ctypes.c_int
     L.laga_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.laga_attn_bwd_stage.restype = ctypes.c_int
+    L.laga_attn_bwd_stage.argtypes = [ctypes.c_int, P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                      ctypes.c_size_t, vp]
     return L
 
 
@@ -181,14 +185,21 @@ def laga_attn_fwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv=None, out=None, lse=None
     return out, lse
 
 
-def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None, dc_kv=None,
-                  dk_pe=None, dw_kv_b=None, workspace=None, stream=None):
-    """Backward of the block; returns (dq, dc_kv, dk_pe, dw_kv_b) — dq in the element
-    dtype, the head-shard partials dc_kv / dk_pe and dw_kv_b in fp32."""
+def _bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe, dw_kv_b, workspace):
     sh, dt = p.shapes(), p.torch_dtype
-    dev = q.device
+    return (ctypes.byref(p.c()), _ptr(q, "q", sh["q"], dt), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
+            _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
+            _ptr(kv, "kv", sh["kv"], dt, required=False), _ptr(out, "out", sh["out"], dt),
+            _ptr(lse, "lse", sh["lse"], torch.float32), _ptr(dout, "dout", sh["dout"], dt),
+            _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], torch.float32),
+            _ptr(dk_pe, "dk_pe", sh["dk_pe"], torch.float32),
+            _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
+            _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size())
+
+
+def _bwd_outputs(p, dev, dq, dc_kv, dk_pe, dw_kv_b, workspace):
     if dq is None:
-        dq = _new(p, "dq", dt, dev)
+        dq = _new(p, "dq", p.torch_dtype, dev)
     if dc_kv is None:
         dc_kv = _new(p, "dc_kv", torch.float32, dev)
     if dk_pe is None:
@@ -196,13 +207,23 @@ def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None
     if dw_kv_b is None:
         dw_kv_b = _new(p, "dw_kv_b", torch.float32, dev)
     workspace = _workspace(p, OP_BWD, workspace, dev)
-    _check(_lib.laga_attn_bwd(
-        ctypes.byref(p.c()), _ptr(q, "q", sh["q"], dt), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
-        _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(w_kv_b, "w_kv_b", sh["w_kv_b"], dt),
-        _ptr(kv, "kv", sh["kv"], dt, required=False), _ptr(out, "out", sh["out"], dt),
-        _ptr(lse, "lse", sh["lse"], torch.float32), _ptr(dout, "dout", sh["dout"], dt),
-        _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], torch.float32),
-        _ptr(dk_pe, "dk_pe", sh["dk_pe"], torch.float32), _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
-        _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)),
-        "laga_attn_bwd")
+    return dq, dc_kv, dk_pe, dw_kv_b, workspace
+
+
+def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None, dc_kv=None,
+                  dk_pe=None, dw_kv_b=None, workspace=None, stream=None):
+    """Backward of the block; returns (dq, dc_kv, dk_pe, dw_kv_b) — dq in the element
+    dtype, the head-shard partials dc_kv / dk_pe and dw_kv_b in fp32."""
+    dq, dc_kv, dk_pe, dw_kv_b, workspace = _bwd_outputs(p, q.device, dq, dc_kv, dk_pe, dw_kv_b, workspace)
+    _check(_lib.laga_attn_bwd(*_bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe,
+                                         dw_kv_b, workspace), _stream(stream)), "laga_attn_bwd")
     return dq, dc_kv, dk_pe, dw_kv_b
+
+
+def laga_attn_bwd_stage(stage: int, p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv,
+                        dk_pe, dw_kv_b, workspace, stream=None):
+    """One stage of laga_attn_bwd (BWD_PREPARE, BWD_DKDV, BWD_DQ, BWD_FINISH); all buffers
+    must be supplied and be the same for every stage of one backward."""
+    _check(_lib.laga_attn_bwd_stage(stage, *_bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq,
+                                                       dc_kv, dk_pe, dw_kv_b, workspace), _stream(stream)),
+           "laga_attn_bwd_stage")

@@ -1,6 +1,7 @@
 """Compile the gfx950 HIP sources into the in-tree shared library liblaga.so.
 
-Usage: python -m paper_2607_17644_amd.build   (or paper_2607_17644_amd.build.build())
+Usage: python paper_2607_17644_amd/build.py   (standalone: it does not import the package,
+whose import needs the built library)
 Every call recompiles (sources are few and hipcc is fast); objects go to
 paper_2607_17644_amd/_build/, the library to paper_2607_17644_amd/liblaga.so.
 """

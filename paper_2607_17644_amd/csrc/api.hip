@@ -145,13 +145,14 @@ laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q, const void* 
   return from_hip(bf ? launch_attn_fwd<bf16, 32, 16, 32>(a, st) : launch_attn_fwd<float, 32, 16, 32>(a, st));
 }
 
-laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
-                            const void* w_kv_b, const void* kv, const void* out, const float* lse,
-                            const void* dout, void* dq, float* dc_kv, float* dk_pe, float* dw_kv_b,
-                            void* workspace, size_t workspace_bytes, void* stream) {
+laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void* q, const void* c_kv,
+                                  const void* k_pe, const void* w_kv_b, const void* kv, const void* out,
+                                  const float* lse, const void* dout, void* dq, float* dc_kv, float* dk_pe,
+                                  float* dw_kv_b, void* workspace, size_t workspace_bytes, void* stream) {
   Dims d;
   laga_status_t s = validate(p, &d);
   if (s != LAGA_OK) return s;
+  if (stage < LAGA_BWD_PREPARE || stage > LAGA_BWD_FINISH) return LAGA_ERR_UNSUPPORTED;
   const bool fused = p->kv_mode == LAGA_KV_FUSED;
   if (!q || !c_kv || !k_pe || !w_kv_b || !out || !lse || !dout || !dq || !dc_kv || !dk_pe || !dw_kv_b ||
       (!fused && !kv))
@@ -169,36 +170,51 @@ laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* 
   const bool v3 = is_v3(p);
 
   if (fused && !kv) {
-    // K/V are rebuilt (same GEMM as laga_reconstruct_kv) into the workspace.
+    // K/V are rebuilt (same GEMM as laga_reconstruct_kv) into the workspace in the first stage.
     void* kvw = wsb + ws.kv;
-    s = bf ? reconstruct_t<bf16>(d, c_kv, w_kv_b, kvw, st) : reconstruct_t<float>(d, c_kv, w_kv_b, kvw, st);
-    if (s != LAGA_OK) return s;
+    if (stage == LAGA_BWD_PREPARE) {
+      s = bf ? reconstruct_t<bf16>(d, c_kv, w_kv_b, kvw, st) : reconstruct_t<float>(d, c_kv, w_kv_b, kvw, st);
+      if (s != LAGA_OK) return s;
+    }
     kv = kvw;
   }
   AttnBwdArgs a{};
   a.q = q; a.k_pe = k_pe; a.kv = kv; a.out = out; a.dout = dout; a.lse = lse; a.dq = dq;
   a.delta = (float*)(wsb + ws.delta); a.dkv = wsb + ws.dkv; a.dkpe_h = (float*)(wsb + ws.dkpe_h);
   a.dkv_lo = bf ? wsb + ws.dkv_lo : nullptr;
-  a.dk_pe = (float*)dk_pe;
+  a.dk_pe = dk_pe;
   a.B = d.B; a.S = d.S; a.H = d.H; a.scale = p->softmax_scale; a.causal = p->causal;
   hipError_t e;
-  if (v3) e = bf ? launch_attn_bwd<bf16, 128, 64, 128>(a, st) : launch_attn_bwd<float, 128, 64, 128>(a, st);
-  else e = bf ? launch_attn_bwd<bf16, 32, 16, 32>(a, st) : launch_attn_bwd<float, 32, 16, 32>(a, st);
-  if (e != hipSuccess) return LAGA_ERR_DEVICE;
+  const int kstage = stage == LAGA_BWD_PREPARE ? 0 : stage == LAGA_BWD_DKDV ? 1 : stage == LAGA_BWD_DQ ? 2 : 3;
+  if (v3) e = bf ? launch_attn_bwd<bf16, 128, 64, 128>(a, kstage, st) : launch_attn_bwd<float, 128, 64, 128>(a, kstage, st);
+  else e = bf ? launch_attn_bwd<bf16, 32, 16, 32>(a, kstage, st) : launch_attn_bwd<float, 32, 16, 32>(a, kstage, st);
+  if (e != hipSuccess || stage != LAGA_BWD_FINISH) return from_hip(e);
 
   const int tok = d.B * d.S, ncol = d.H * d.dkvh();
   float* part = (float*)(wsb + ws.dw_part);
   if (bf) {
     const bf16* hi = (const bf16*)a.dkv;
     const bf16* lo = (const bf16*)a.dkv_lo;
-    e = launch_dc<bf16>(hi, lo, (const bf16*)w_kv_b, (float*)dc_kv, tok, d.d_c, ncol, st);
+    e = launch_dc<bf16>(hi, lo, (const bf16*)w_kv_b, dc_kv, tok, d.d_c, ncol, st);
     if (e == hipSuccess) e = launch_dw<bf16>((const bf16*)c_kv, hi, lo, dw_kv_b, part, d.d_c, ncol, tok, st);
   } else {
     const float* g = (const float*)a.dkv;
-    e = launch_dc<float>(g, nullptr, (const float*)w_kv_b, (float*)dc_kv, tok, d.d_c, ncol, st);
+    e = launch_dc<float>(g, nullptr, (const float*)w_kv_b, dc_kv, tok, d.d_c, ncol, st);
     if (e == hipSuccess) e = launch_dw<float>((const float*)c_kv, g, nullptr, dw_kv_b, part, d.d_c, ncol, tok, st);
   }
   return from_hip(e);
+}
+
+laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
+                            const void* w_kv_b, const void* kv, const void* out, const float* lse,
+                            const void* dout, void* dq, float* dc_kv, float* dk_pe, float* dw_kv_b,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  for (int stage = LAGA_BWD_PREPARE; stage <= LAGA_BWD_FINISH; ++stage) {
+    laga_status_t s = laga_attn_bwd_stage(stage, p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe,
+                                          dw_kv_b, workspace, workspace_bytes, stream);
+    if (s != LAGA_OK) return s;
+  }
+  return LAGA_OK;
 }
 
 }  // extern "C"

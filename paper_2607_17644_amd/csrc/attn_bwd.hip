@@ -60,26 +60,39 @@ struct BwdParams {
   int causal;
 };
 
+// delta[b,h,t] = sum_e dout[b,t,h,e] * out[b,t,h,e]. One wave per token: the token's
+// [H, DV] rows of out and dout are contiguous, lanes read consecutive 16-byte chunks,
+// and the DV/E lanes that share a head finish the sum with xor shuffles.
 template <typename T, int DV>
 __global__ __launch_bounds__(256) void delta_kernel(const T* __restrict__ out, const T* __restrict__ dout,
-                                                    float* __restrict__ delta, int S, int H, int BSH) {
-  const int i = blockIdx.x * 256 + threadIdx.x;  // (b*S + t)*H + h
-  if (i >= BSH) return;
-  constexpr int E = Elems16<T>::n;
-  const T* o = out + (size_t)i * DV;
-  const T* d = dout + (size_t)i * DV;
-  float acc = 0.f;
+                                                    float* __restrict__ delta, int S, int H, int BS) {
+  constexpr int E = Elems16<T>::n, CPH = DV / E;  // chunks per head (a power of two dividing 64)
+  static_assert(64 % CPH == 0, "heads must tile the wave");
+  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
+  if (tok >= BS) return;
+  const int nch = H * CPH;
+  const T* o = out + (size_t)tok * H * DV;
+  const T* d = dout + (size_t)tok * H * DV;
+  const int b = tok / S, t = tok % S;
+  for (int c0 = 0; c0 < nch; c0 += 64) {  // wave-uniform trip count
+    const int c = c0 + l;
+    float acc = 0.f;
+    if (c < nch) {
+      chunk16 va = *reinterpret_cast<const chunk16*>(o + (size_t)c * E);
+      chunk16 vb = *reinterpret_cast<const chunk16*>(d + (size_t)c * E);
+      const T* pa = reinterpret_cast<const T*>(&va);
+      const T* pb = reinterpret_cast<const T*>(&vb);
 #pragma unroll
-  for (int c = 0; c < DV; c += E) {
-    chunk16 a = *reinterpret_cast<const chunk16*>(o + c);
-    chunk16 b = *reinterpret_cast<const chunk16*>(d + c);
-    const T* pa = reinterpret_cast<const T*>(&a);
-    const T* pb = reinterpret_cast<const T*>(&b);
+      for (int e = 0; e < E; ++e) acc += to_f32(pa[e]) * to_f32(pb[e]);
+    }
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc += to_f32(pa[e]) * to_f32(pb[e]);
+    for (int m = 1; m < CPH; m <<= 1) acc += __shfl_xor(acc, m);
+    if (c < nch && (c % CPH) == 0) {
+      const int h = c / CPH;
+      delta[(size_t)(b * H + h) * S + t] = acc;
+    }
   }
-  const int h = i % H, bt = i / H, b = bt / S, t = bt % S;
-  delta[(size_t)(b * H + h) * S + t] = acc;
 }
 
 // ------------------------------------------------------------------ dK, dV
@@ -453,30 +466,31 @@ template <> struct BwdTiles<float> { static constexpr int BQ = 32, BC = 32, WPH_
 }  // namespace
 
 template <typename T, int DN, int DR, int DV>
-hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t st) {
+hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
   using Tl = BwdTiles<T>;
-  const int BSH = a.B * a.S * a.H;
-  delta_kernel<T, DV><<<(BSH + 255) / 256, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.delta, a.S, a.H, BSH);
-
   BwdParams P;
   P.q = a.q; P.k_pe = a.k_pe; P.kv = a.kv; P.dout = a.dout; P.lse = a.lse; P.delta = a.delta;
   P.dq = a.dq; P.dkv = a.dkv; P.dkv_lo = a.dkv_lo; P.dkpe_h = a.dkpe_h;
   P.S = a.S; P.H = a.H; P.scale = a.scale; P.scale_log2 = a.scale * 1.4426950408889634f; P.causal = a.causal;
-
-  constexpr int BK = 32 * Tl::WPH_KV;
-  P.n_blocks = (a.S + BK - 1) / BK;
-  dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
-
-  constexpr int BR = 32 * Tl::WPH_Q;
-  P.n_blocks = (a.S + BR - 1) / BR;
-  dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_Q, 0, st>>>(P);
-
-  const int n4 = a.B * a.S * DR / 4;
-  dkpe_kernel<DR><<<(n4 + 255) / 256, 256, 0, st>>>(a.dkpe_h, a.dk_pe, a.H, n4);
+  if (stage == 0) {
+    const int BS = a.B * a.S;
+    delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.delta, a.S, a.H, BS);
+  } else if (stage == 1) {
+    constexpr int BK = 32 * Tl::WPH_KV;
+    P.n_blocks = (a.S + BK - 1) / BK;
+    dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+  } else if (stage == 2) {
+    constexpr int BR = 32 * Tl::WPH_Q;
+    P.n_blocks = (a.S + BR - 1) / BR;
+    dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_Q, 0, st>>>(P);
+  } else {
+    const int n4 = a.B * a.S * DR / 4;
+    dkpe_kernel<DR><<<(n4 + 255) / 256, 256, 0, st>>>(a.dkpe_h, a.dk_pe, a.H, n4);
+  }
   return hipGetLastError();
 }
 
-#define LAGA_INST_BWD(T, DN, DR, DV) template hipError_t launch_attn_bwd<T, DN, DR, DV>(const AttnBwdArgs&, hipStream_t);
+#define LAGA_INST_BWD(T, DN, DR, DV) template hipError_t launch_attn_bwd<T, DN, DR, DV>(const AttnBwdArgs&, int, hipStream_t);
 LAGA_INST_BWD(bf16, 128, 64, 128)
 LAGA_INST_BWD(float, 128, 64, 128)
 LAGA_INST_BWD(bf16, 32, 16, 32)

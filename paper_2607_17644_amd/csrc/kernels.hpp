@@ -53,8 +53,9 @@ struct AttnBwdArgs {
   int causal;
 };
 
-// delta, dK/dV (into dkv, dkpe_h), dQ and the dk_pe head sum; dc_kv / dW are the GEMMs above.
+// stage 0: delta; 1: dK/dV (into dkv, dkpe_h); 2: dQ; 3: dk_pe head sum.
+// (dc_kv / dW are the GEMMs above.)
 template <typename T, int DN, int DR, int DV>
-hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t st);
+hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st);
 
 }  // namespace laga

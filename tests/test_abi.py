@@ -79,3 +79,10 @@ def test_attention_entry_points_validate_first():
     st = lib.laga_attn_bwd(ctypes.byref(P.c()), fake, fake, fake, fake, fake, fake, fake, fake,
                            fake, fake, fake, fake, fake, need - 1, z)
     assert st == 5
+    # stage entry point: unknown stage -> unsupported, before touching anything
+    st = lib.laga_attn_bwd_stage(7, ctypes.byref(P.c()), fake, fake, fake, fake, fake, fake, fake, fake,
+                                 fake, fake, fake, fake, fake, need, z)
+    assert st == 3
+    st = lib.laga_attn_bwd_stage(1, ctypes.byref(P.c()), fake, fake, fake, fake, fake, fake, fake, fake,
+                                 fake, fake, fake, fake, fake, need - 1, z)
+    assert st == 5
