@@ -70,9 +70,10 @@ BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   return w;
 }
 
+// Forward workspace: the fused mode keeps W_kv_b^T (H*(d_nope+d_v) x d_c) there.
 size_t fwd_ws_bytes(const laga_problem_t* p, const Dims& d) {
-  (void)p; (void)d;
-  return 0;
+  if (p->kv_mode != LAGA_KV_FUSED) return 0;
+  return round_up(elem_size(p) * (size_t)d.d_c * d.H * d.dkvh());
 }
 
 laga_status_t from_hip(hipError_t e) { return e == hipSuccess ? LAGA_OK : LAGA_ERR_DEVICE; }
@@ -135,12 +136,19 @@ laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q, const void* 
   const size_t need = fwd_ws_bytes(p, d);
   if (need > 0 && (!workspace || workspace_bytes < need)) return LAGA_ERR_WORKSPACE;
   if (need > 0 && misaligned(workspace)) return LAGA_ERR_ALIGN;
-  if (fused) return LAGA_ERR_UNSUPPORTED;
+  if (fused && d.d_c > kFusedMaxDc) return LAGA_ERR_UNSUPPORTED;
   AttnFwdArgs a{};
-  a.q = q; a.k_pe = k_pe; a.kv = kv; a.c_kv = c_kv; a.w_t = nullptr; a.out = out; a.lse = lse;
+  a.q = q; a.k_pe = k_pe; a.kv = kv; a.c_kv = c_kv; a.w = w_kv_b; a.out = out; a.lse = lse;
   a.B = d.B; a.S = d.S; a.H = d.H; a.d_c = d.d_c; a.scale = p->softmax_scale; a.causal = p->causal;
   hipStream_t st = (hipStream_t)stream;
   const bool bf = p->dtype == LAGA_DTYPE_BF16;
+  if (fused) {
+    if (is_v3(p))
+      return from_hip(bf ? launch_attn_fwd_fused<bf16, 128, 64, 128>(a, workspace, st)
+                         : launch_attn_fwd_fused<float, 128, 64, 128>(a, workspace, st));
+    return from_hip(bf ? launch_attn_fwd_fused<bf16, 32, 16, 32>(a, workspace, st)
+                       : launch_attn_fwd_fused<float, 32, 16, 32>(a, workspace, st));
+  }
   if (is_v3(p)) return from_hip(bf ? launch_attn_fwd<bf16, 128, 64, 128>(a, st) : launch_attn_fwd<float, 128, 64, 128>(a, st));
   return from_hip(bf ? launch_attn_fwd<bf16, 32, 16, 32>(a, st) : launch_attn_fwd<float, 32, 16, 32>(a, st));
 }

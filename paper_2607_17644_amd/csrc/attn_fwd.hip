@@ -54,6 +54,81 @@ struct FwdParams {
   int causal;
 };
 
+// One key tile of the online-softmax forward for one wave (32 queries, one head):
+// S^T = K Q^T from the LDS K_nope / k_pe tiles, masked base-2 softmax update of
+// (m, lsum, O^T), then O^T += V^T P^T with V^T read by transposing LDS reads.
+template <typename T, int DN, int DR, int DV, int BC>
+__device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int PP, const T* sVh, int PV,
+                                         const frag_t<T> (&qf)[(DN + DR) / 16], f32x16 (&oacc)[DV / 32], float& m,
+                                         float& lsum, int kt, int q0, int my_q, int S, float scale_log2, int causal,
+                                         bool head_ok) {
+  constexpr int DQK = DN + DR;
+  const int l = threadIdx.x & 63, n = l & 31, g = l >> 5;
+  const bool active = head_ok && q0 < S && (!causal || kt <= q0 + 31);
+  if (!active) return;
+
+  f32x16 sacc[BC / 32];
+#pragma unroll
+  for (int kb = 0; kb < BC / 32; ++kb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      const frag_t<T> a = ks < DN / 16
+          ? lds_frag<T>(sKh + (kb * 32 + n) * PK + ks * 16 + 8 * g)
+          : lds_frag<T>(sP + (kb * 32 + n) * PP + (ks - DN / 16) * 16 + 8 * g);
+      mma(sacc[kb], a, qf[ks]);
+    }
+  }
+
+  // scale (base 2) and mask; only tiles crossing the diagonal or the end need the mask
+  const bool need_mask = (causal && kt + BC - 1 > q0) || (kt + BC > S);
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float s = sacc[kb][r] * scale_log2;
+      if (need_mask) {
+        const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        if (key >= S || (causal && key > my_q)) s = -INFINITY;
+      }
+      sacc[kb][r] = s;
+      mloc = fmaxf(mloc, s);
+    }
+  mloc = wave_xor32_max(mloc);
+  const float m_new = fmaxf(m, mloc);
+  const float m_use = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = fast_exp2(m - m_use);
+  float ps = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = fast_exp2(sacc[kb][r] - m_use);
+      sacc[kb][r] = p;
+      ps += p;
+    }
+  lsum = lsum * alpha + ps;
+  m = m_new;
+#pragma unroll
+  for (int i = 0; i < DV / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+
+  frag_t<T> pf[BC / 16];
+#pragma unroll
+  for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
+#pragma unroll
+  for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+    for (int kk = 0; kk < BC / 16; ++kk) {
+      const int ra = kk * 16 + 4 * g;
+      const frag_t<T> a = TrRead<T>::get(sVh, PV, ra, ra + 8, db * 32);
+      mma(oacc[db], a, pf[kk]);
+    }
+}
+
 template <typename T, int DN, int DR, int DV, int BC, int WPH, int G, bool FUSED>
 __global__ __launch_bounds__(64 * WPH * G)
 void attn_fwd_kernel(FwdParams P) {
@@ -158,69 +233,8 @@ void attn_fwd_kernel(FwdParams P) {
     __syncthreads();
     if (kt + BC < kend) load_tile(kt + BC);  // prefetch overlaps the math below
 
-    const bool active = head_ok && q0 < S && (!P.causal || kt <= q0 + 31);
-    if (!active) continue;
-
-    f32x16 sacc[BC / 32];
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < DQK / 16; ++ks) {
-        const frag_t<T> a = ks < DN / 16
-            ? lds_frag<T>(sKh + (kb * 32 + n) * C::PK + ks * 16 + 8 * g)
-            : lds_frag<T>(sP + (kb * 32 + n) * C::PP + (ks - DN / 16) * 16 + 8 * g);
-        mma(sacc[kb], a, qf[ks]);
-      }
-    }
-
-    // scale (base 2) and mask; only tiles crossing the diagonal or the end need the mask
-    const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float s = sacc[kb][r] * P.scale_log2;
-        if (need_mask) {
-          const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (key >= S || (P.causal && key > my_q)) s = -INFINITY;
-        }
-        sacc[kb][r] = s;
-        mloc = fmaxf(mloc, s);
-      }
-    mloc = wave_xor32_max(mloc);
-    const float m_new = fmaxf(m, mloc);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m - m_use);
-    float ps = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(sacc[kb][r] - m_use);
-        sacc[kb][r] = p;
-        ps += p;
-      }
-    lsum = lsum * alpha + ps;
-    m = m_new;
-#pragma unroll
-    for (int i = 0; i < DV / 32; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
-
-    frag_t<T> pf[BC / 16];
-#pragma unroll
-    for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
-#pragma unroll
-    for (int db = 0; db < DV / 32; ++db)
-#pragma unroll
-      for (int kk = 0; kk < BC / 16; ++kk) {
-        const int ra = kk * 16 + 4 * g;
-        const frag_t<T> a = TrRead<T>::get(sVh, C::PV, ra, ra + 8, db * 32);
-        mma(oacc[db], a, pf[kk]);
-      }
+    fwd_tile<T, DN, DR, DV, BC>(sKh, C::PK, sP, C::PP, sVh, C::PV, qf, oacc, m, lsum, kt, q0, my_q, S,
+                                P.scale_log2, P.causal, head_ok);
   }
 
   if (!head_ok || my_q >= S) return;
@@ -237,6 +251,205 @@ void attn_fwd_kernel(FwdParams P) {
       *reinterpret_cast<typename FragOf<T>::half*>(orow + db * 32 + rr * 8 + g * 4) = v;
     }
   if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
+}
+
+
+// ------------------------------------------------------------------ fused variant
+// No per-head K/V tensor exists in HBM. For each key tile the latent rows
+// c_kv[kt : kt+BC, :] are copied straight into LDS (direct global->LDS loads, one
+// row per wave instruction and 64-chunk segment), and the head's K_nope / V tile is
+// rebuilt on chip as KV^T = W_h^T c^T: the A operand is the transposed weight
+// (w_t [H*(DN+DV), d_c], read from global / L2), the B operand the LDS latent rows.
+// Shape, operand roles and contraction order (ascending 16-wide steps over d_c from
+// a zero accumulator) are those of the up-projection GEMM, and the result is rounded
+// to the element type the same way, so the rebuilt tile equals the materialised kv
+// bit for bit. The attention part is fwd_tile, unchanged.
+struct FwdFusedParams {
+  const void* q;
+  const void* k_pe;
+  const void* c_kv;
+  const void* w_t;
+  void* out;
+  float* lse;
+  int S, H, d_c, n_qblocks;
+  float scale_log2;
+  int causal;
+};
+
+// Latent rows [kt, kt+nrows) of batch b -> sC (row pitch `pitch` elements): direct
+// global->LDS loads, one wave instruction per row and 64-chunk segment (lane l lands
+// 16*l bytes after the segment start); rows past S are zero-filled by LDS stores.
+template <typename T>
+__device__ __forceinline__ void load_latent_rows(const T* __restrict__ cg, T* sC, int nrows, int pitch, int nw,
+                                                 int b, int S, int dc, int kt, int wave, int l) {
+  constexpr int E = Elems16<T>::n;
+  const int row_chunks = dc / E;
+  for (int row = wave; row < nrows; row += nw) {
+    const int key = kt + row;
+    T* dst = sC + row * pitch;
+    for (int seg = 0; seg < row_chunks; seg += 64) {
+      const int c = seg + l;
+      if (c < row_chunks) {
+        if (key < S) g2lds16(cg + ((size_t)(b * S + key) * dc + (size_t)c * E), dst + seg * E);
+        else *reinterpret_cast<chunk16*>(dst + c * E) = zero_chunk();
+      }
+    }
+  }
+}
+
+template <typename T, int DN, int DR, int DV, int BC, int WPH, int DCMAX>
+__global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams P) {
+  constexpr int DQK = DN + DR, DKVH = DN + DV, E = Elems16<T>::n, NT = 64 * WPH, NW = WPH;
+  constexpr int PK = DN + 8, PP = DR + 8, PV = DV + 32 / (int)sizeof(T), PC = DCMAX + 8;
+  constexpr int NCBLK = DKVH / 32, NKB = BC / 32;
+  constexpr int NCB = NCBLK >= NW ? NCBLK / NW : 1;  // column blocks rebuilt per wave
+  static_assert(NCBLK % NW == 0 || NCBLK < NW, "column blocks must split over the waves");
+  __shared__ __attribute__((aligned(16))) T sK[BC * PK];
+  __shared__ __attribute__((aligned(16))) T sP[BC * PP];
+  __shared__ __attribute__((aligned(16))) T sV[BC * PV];
+  __shared__ __attribute__((aligned(16))) T sC[BC * PC];
+
+  const T* __restrict__ q = (const T*)P.q;
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ cg = (const T*)P.c_kv;
+  const T* __restrict__ wt = (const T*)P.w_t;
+  const int S = P.S, H = P.H, dc = P.d_c;
+
+  const int total = P.n_qblocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int qb = P.n_qblocks - 1 - lin % P.n_qblocks;
+  const int bh = lin / P.n_qblocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
+  const int q0 = qb * 32 * WPH + wave * 32;
+  const int my_q = q0 + n;
+  const int wg_qend = min(S, (qb + 1) * 32 * WPH);
+  const int kend = P.causal ? wg_qend : S;
+
+  frag_t<T> qf[DQK / 16];
+  {
+    const bool ok = my_q < S;
+    const T* qrow = q + ((size_t)(b * S + (ok ? my_q : 0)) * H + h) * DQK;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      if (ok) qf[ks] = *reinterpret_cast<const frag_t<T>*>(qrow + ks * 16 + 8 * g);
+      else
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[ks][e] = to_elem<T>(0.f);
+    }
+  }
+  f32x16 oacc[DV / 32];
+#pragma unroll
+  for (int i = 0; i < DV / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+
+  // k_pe tile -> sP (through registers; small)
+  constexpr int PCH = BC * (DR / E);
+  constexpr int PPT = (PCH + NT - 1) / NT;
+  chunk16 pst[PPT];
+  auto load_p = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int c = tid + i * NT;
+      pst[i] = zero_chunk();
+      if (c < PCH) {
+        const int row = c / (DR / E), j = c % (DR / E);
+        if (kt + row < S) pst[i] = *reinterpret_cast<const chunk16*>(kpe + (size_t)(b * S + kt + row) * DR + j * E);
+      }
+    }
+  };
+  auto store_p = [&]() {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < PCH) {
+        const int row = c / (DR / E), j = c % (DR / E);
+        *reinterpret_cast<chunk16*>(sP + row * PP + j * E) = pst[i];
+      }
+    }
+  };
+
+  load_latent_rows<T>(cg, sC, BC, PC, NW, b, S, dc, 0, wave, l);
+  load_p(0);
+  for (int kt = 0; kt < kend; kt += BC) {
+    wait_vmem();                    // this wave's direct loads into sC have landed
+    __syncthreads();                // all of sC present; previous tile's sK/sV/sP consumed
+    store_p();
+    // rebuild K_nope / V of this tile: KV^T[col][key] = sum_c W^T[col][c] * c[key][c]
+    const int cb0 = wave * NCB;
+    if (cb0 < NCBLK) {
+      f32x16 acc[NCB][NKB];
+#pragma unroll
+      for (int i = 0; i < NCB; ++i)
+#pragma unroll
+        for (int j = 0; j < NKB; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      const T* wrow[NCB];
+#pragma unroll
+      for (int i = 0; i < NCB; ++i) wrow[i] = wt + (size_t)(h * DKVH + (cb0 + i) * 32 + n) * dc + 8 * g;
+      for (int ks = 0; ks < dc / 16; ++ks) {
+        frag_t<T> a[NCB], bb[NKB];
+#pragma unroll
+        for (int i = 0; i < NCB; ++i) a[i] = *reinterpret_cast<const frag_t<T>*>(wrow[i] + ks * 16);
+#pragma unroll
+        for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
+#pragma unroll
+        for (int i = 0; i < NCB; ++i)
+#pragma unroll
+          for (int j = 0; j < NKB; ++j) mma(acc[i][j], a[i], bb[j]);
+      }
+#pragma unroll
+      for (int i = 0; i < NCB; ++i)
+#pragma unroll
+        for (int j = 0; j < NKB; ++j)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int col = (cb0 + i) * 32 + rr * 8 + g * 4;
+            const int key = j * 32 + n;
+            typename FragOf<T>::half v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(acc[i][j][4 * rr + e]);
+            T* dst = col < DN ? sK + key * PK + col : sV + key * PV + (col - DN);
+            *reinterpret_cast<typename FragOf<T>::half*>(dst) = v;
+          }
+    }
+    __syncthreads();  // sK / sV / sP complete; sC free
+    if (kt + BC < kend) {
+      load_latent_rows<T>(cg, sC, BC, PC, NW, b, S, dc, kt + BC, wave, l);
+      load_p(kt + BC);
+    }
+    fwd_tile<T, DN, DR, DV, BC>(sK, PK, sP, PP, sV, PV, qf, oacc, m, lsum, kt, q0, my_q, S, P.scale_log2,
+                                P.causal, true);
+    __syncthreads();  // everyone done reading sK / sV / sP before the next rebuild
+  }
+
+  if (my_q >= S) return;
+  const float ltot = wave_xor32_sum(lsum);
+  const float inv = 1.f / ltot;
+  T* orow = (T*)P.out + ((size_t)(b * S + my_q) * H + h) * DV;
+#pragma unroll
+  for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      typename FragOf<T>::half v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(oacc[db][4 * rr + e] * inv);
+      *reinterpret_cast<typename FragOf<T>::half*>(orow + db * 32 + rr * 8 + g * 4) = v;
+    }
+  if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
+}
+
+// w_t[n][k] = w[k][n]  (K = d_c rows, N = H*(DN+DV) columns), one thread per output element
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_w_kernel(const T* __restrict__ w, T* __restrict__ w_t, int K, int N) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * N) return;
+  const int n = (int)(i / K), k = (int)(i % K);
+  w_t[i] = w[(size_t)k * N + n];
 }
 
 template <typename T, int DN, int DR, int DV> struct FwdTiles;
@@ -266,7 +479,26 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-#define LAGA_INST_FWD(T, DN, DR, DV) template hipError_t launch_attn_fwd<T, DN, DR, DV>(const AttnFwdArgs&, hipStream_t);
+template <typename T, int DN, int DR, int DV>
+hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t st) {
+  using Tl = FwdTiles<T, DN, DR, DV>;
+  constexpr int BR = 32 * Tl::WPH;
+  const int N = a.H * (DN + DV);
+  const long long nw = (long long)a.d_c * N;
+  transpose_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
+  FwdFusedParams P;
+  P.q = a.q; P.k_pe = a.k_pe; P.c_kv = a.c_kv; P.w_t = w_t_ws; P.out = a.out; P.lse = a.lse;
+  P.S = a.S; P.H = a.H; P.d_c = a.d_c; P.n_qblocks = (a.S + BR - 1) / BR;
+  P.scale_log2 = a.scale * 1.4426950408889634f;
+  P.causal = a.causal;
+  dim3 grid(P.n_qblocks * a.H, a.B, 1);
+  attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, kFusedMaxDc><<<grid, 64 * Tl::WPH, 0, st>>>(P);
+  return hipGetLastError();
+}
+
+#define LAGA_INST_FWD(T, DN, DR, DV)                                                      \
+  template hipError_t launch_attn_fwd<T, DN, DR, DV>(const AttnFwdArgs&, hipStream_t);    \
+  template hipError_t launch_attn_fwd_fused<T, DN, DR, DV>(const AttnFwdArgs&, void*, hipStream_t);
 LAGA_INST_FWD(bf16, 128, 64, 128)
 LAGA_INST_FWD(float, 128, 64, 128)
 LAGA_INST_FWD(bf16, 32, 16, 32)

@@ -107,6 +107,17 @@ __device__ __forceinline__ float wave_xor32_sum(float x) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
+// lane l's 16 bytes from `g` land at LDS address lds + 16 * l, where `lds` must be
+// the same for every lane of the wave. Tracked by vmcnt like any global load.
+__device__ __forceinline__ void g2lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+
+// Wait until all of this wave's outstanding vector-memory loads (including direct
+// global -> LDS copies) have completed.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Zero value of a 16-byte staging chunk.
 __device__ __forceinline__ chunk16 zero_chunk() { chunk16 z = {0, 0, 0, 0}; return z; }
 

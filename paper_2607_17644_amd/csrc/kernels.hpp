@@ -24,7 +24,7 @@ struct AttnFwdArgs {
   const void* k_pe;   // [B,S,DR]
   const void* kv;     // [B,S,H,DN+DV] (materialised path)
   const void* c_kv;   // [B,S,d_c]     (fused path)
-  const void* w_t;    // [H*(DN+DV), d_c] transposed W_kv_b (fused path)
+  const void* w;      // [d_c, H*(DN+DV)] W_kv_b (fused path)
   void* out;          // [B,S,H,DV]
   float* lse;         // [B,H,S]
   int B, S, H, d_c;
@@ -34,6 +34,12 @@ struct AttnFwdArgs {
 
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
+
+// Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T
+// (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
+constexpr int kFusedMaxDc = 512;
+template <typename T, int DN, int DR, int DV>
+hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t st);
 
 struct AttnBwdArgs {
   const void* q;

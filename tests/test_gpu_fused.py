@@ -1,0 +1,59 @@
+"""Fused latent->LDS forward (K/V rebuilt on chip, never written to HBM) through the C ABI.
+
+The rebuild uses the up-projection GEMM's MFMA shape, operand roles and contraction
+order, so its K/V tiles - and hence out and lse - equal the materialised path bit for bit;
+the oracle comparison is implied by the materialised tests and repeated here."""
+import pytest
+
+import laga_inputs as LI
+from oracle import laga as O
+from _util import TOL, dev_inputs, f64, problem_for, scaled_err
+
+pytestmark = pytest.mark.gpu
+
+
+def both(w):
+    import paper_2607_17644_amd as L
+    x = LI.make_inputs(w, with_dout=False)
+    d = dev_inputs(w, x)
+    p = problem_for(w)
+    kv = L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"])
+    om, lm = L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv)
+    pf = problem_for(w, kv_mode=L.KV_FUSED)
+    of, lf = L.laga_attn_fwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"])
+    return x, om, lm, of, lf
+
+
+@pytest.mark.parametrize("name,S,H,B,causal", [
+    ("tiny_fp32", 256, 4, 1, True), ("tiny_fp32", 45, 4, 2, False), ("tiny_fp32", 7, 4, 1, True),
+    ("v3_shard_s4096", 4096, 16, 1, True), ("v3_shard_s4096", 300, 3, 2, True),
+    ("v3_shard_s4096", 1, 1, 1, True), ("v3_shard_s4096", 257, 2, 1, False)])
+def test_fused_equals_materialised_bitwise(name, S, H, B, causal):
+    import torch
+    w = LI.WORKLOADS[name].replace(seq_len=S, n_heads=H, batch=B, causal=causal)
+    x, om, lm, of, lf = both(w)
+    assert torch.equal(om, of) and torch.equal(lm, lf)
+    ro, rl = O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], n_heads=H, d_nope=w.d_nope,
+                        d_v=w.d_v, scale=w.scale, causal=causal)
+    assert scaled_err(f64(of), ro) < TOL[w.dtype] and scaled_err(f64(lf), rl) < TOL[w.dtype]
+
+
+def test_fused_s16384_bitwise():
+    """The full-size comparison configuration (S=16384, 16 heads): both paths agree exactly."""
+    import torch
+    w = LI.WORKLOADS["v3_shard_s16384"]
+    _, om, lm, of, lf = both(w)
+    assert torch.equal(om, of) and torch.equal(lm, lf)
+
+
+def test_fused_workspace_and_limits():
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=64)
+    pf = problem_for(w, kv_mode=L.KV_FUSED)
+    assert L.laga_workspace_bytes(pf, L.OP_FWD) >= 512 * 16 * 256 * 2
+    big = problem_for(w.replace(d_c=1024), kv_mode=L.KV_FUSED)
+    x = LI.make_inputs(w.replace(d_c=1024), with_dout=False)
+    d = dev_inputs(w, x)
+    with pytest.raises(L.LagaError) as e:
+        L.laga_attn_fwd(big, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"])
+    assert e.value.status == 3
