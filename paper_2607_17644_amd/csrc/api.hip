@@ -51,15 +51,17 @@ size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ?
 
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Backward workspace: [delta | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials | kv rebuild]
+// Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials | kv rebuild]
 struct BwdWs {
-  size_t delta, dkv, dkv_lo, dkpe_h, dw_part, kv, total;
+  size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, total;
 };
+int s_pad(int S) { return (S + kRowPad - 1) / kRowPad * kRowPad; }
 BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   BwdWs w{};
   const size_t tok = (size_t)d.B * d.S;
   size_t off = 0;
-  w.delta = off; off += round_up(sizeof(float) * tok * d.H);
+  w.delta = off; off += round_up(sizeof(float) * d.B * d.H * s_pad(d.S));
+  w.lse2 = off; off += round_up(sizeof(float) * d.B * d.H * s_pad(d.S));
   w.dkv = off; off += round_up(elem_size(p) * tok * d.H * d.dkvh());
   w.dkv_lo = off; off += p->dtype == LAGA_DTYPE_BF16 ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
   w.dkpe_h = off; off += round_up(sizeof(float) * tok * d.H * d.dr);
@@ -189,6 +191,7 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
   AttnBwdArgs a{};
   a.q = q; a.k_pe = k_pe; a.kv = kv; a.out = out; a.dout = dout; a.lse = lse; a.dq = dq;
   a.delta = (float*)(wsb + ws.delta); a.dkv = wsb + ws.dkv; a.dkpe_h = (float*)(wsb + ws.dkpe_h);
+  a.lse2 = (float*)(wsb + ws.lse2); a.S_pad = s_pad(d.S);
   a.dkv_lo = bf ? wsb + ws.dkv_lo : nullptr;
   a.dk_pe = dk_pe;
   a.B = d.B; a.S = d.S; a.H = d.H; a.scale = p->softmax_scale; a.causal = p->causal;

@@ -50,7 +50,9 @@ struct BwdParams {
   const void* kv;
   const void* dout;
   const float* lse;
-  const float* delta;
+  const float* delta;  // [B*H][S_pad]
+  const float* lse2;   // [B*H][S_pad], lse * log2(e)
+  int S_pad;
   void* dq;
   void* dkv;       // [B,S,H,DN+DV] element dtype
   void* dkv_lo;    // [B,S,H,DN+DV] bf16 low halves (bf16 only; else unused)
@@ -63,9 +65,13 @@ struct BwdParams {
 // delta[b,h,t] = sum_e dout[b,t,h,e] * out[b,t,h,e]. One wave per token: the token's
 // [H, DV] rows of out and dout are contiguous, lanes read consecutive 16-byte chunks,
 // and the DV/E lanes that share a head finish the sum with xor shuffles.
+// Also writes lse2 = lse * log2(e); delta and lse2 rows are [B*H][S_pad] with
+// S_pad = S rounded up to kRowPad, the pad entries zeroed (tiles of the
+// key-stationary kernel are fetched whole).
 template <typename T, int DV>
 __global__ __launch_bounds__(256) void delta_kernel(const T* __restrict__ out, const T* __restrict__ dout,
-                                                    float* __restrict__ delta, int S, int H, int BS) {
+                                                    const float* __restrict__ lse, float* __restrict__ delta,
+                                                    float* __restrict__ lse2, int S, int S_pad, int H, int BS) {
   constexpr int E = Elems16<T>::n, CPH = DV / E;  // chunks per head (a power of two dividing 64)
   static_assert(64 % CPH == 0, "heads must tile the wave");
   const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -90,7 +96,11 @@ __global__ __launch_bounds__(256) void delta_kernel(const T* __restrict__ out, c
     for (int m = 1; m < CPH; m <<= 1) acc += __shfl_xor(acc, m);
     if (c < nch && (c % CPH) == 0) {
       const int h = c / CPH;
-      delta[(size_t)(b * H + h) * S + t] = acc;
+      const size_t o = (size_t)(b * H + h) * S_pad + t;
+      delta[o] = acc;
+      lse2[o] = lse[(size_t)(b * H + h) * S + t] * 1.4426950408889634f;
+      if (t == S - 1)
+        for (int tp = S; tp < S_pad; ++tp) { delta[o + tp - t] = 0.f; lse2[o + tp - t] = 0.f; }
     }
   }
 }
@@ -182,8 +192,8 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
     }
     if (tid < BQ) {
       const int qi = qt + tid;
-      st_l = qi < S ? P.lse[(size_t)(b * H + h) * S + qi] * 1.4426950408889634f : 0.f;
-      st_d = qi < S ? P.delta[(size_t)(b * H + h) * S + qi] : 0.f;
+      st_l = qi < S ? P.lse2[(size_t)(b * H + h) * P.S_pad + qi] : 0.f;
+      st_d = qi < S ? P.delta[(size_t)(b * H + h) * P.S_pad + qi] : 0.f;
     }
   };
   auto store_tile = [&]() {
@@ -291,6 +301,160 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
       put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
 }
 
+
+// Key-stationary backward, bf16 with 192/128-wide heads: the query tiles (Q, dO and
+// the per-row lse2 / delta) stream through a two-stage LDS ring filled by direct
+// global->LDS loads into swizzled, unpadded tiles, so no registers are spent on
+// staging and one barrier per tile suffices. Math as in dkdv_kernel.
+template <int DN, int DR, int DV, int WPH>
+__global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 32 * WPH;
+  constexpr int QCPR = DQK / 8, OCPR = DV / 8;  // 16-byte chunks per row
+  static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
+  __shared__ __attribute__((aligned(16))) T sQ[2][BQ * DQK];
+  __shared__ __attribute__((aligned(16))) T sO[2][BQ * DV];
+  __shared__ __attribute__((aligned(16))) float sLD[2][2 * BQ];  // lse2 then delta
+
+  const T* __restrict__ q = (const T*)P.q;
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ kv = (const T*)P.kv;
+  const T* __restrict__ dout = (const T*)P.dout;
+  const int S = P.S, H = P.H;
+
+  const int total = P.n_blocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int kb = lin % P.n_blocks;
+  const int bh = lin / P.n_blocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
+  const int k0 = kb * BK + wave * 32;
+  const int my_k = k0 + n;
+
+  frag_t<T> kf[DQK / 16], vf[DV / 16];
+  {
+    const bool ok = my_k < S;
+    const size_t row = (size_t)(b * S + (ok ? my_k : 0));
+    const T* kvr = kv + (row * H + h) * DKVH;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      const T* src = ks < DN / 16 ? kvr + ks * 16 + 8 * g : kpe + row * DR + (ks - DN / 16) * 16 + 8 * g;
+      kf[ks] = *reinterpret_cast<const frag_t<T>*>(src);
+      if (!ok) kf[ks] = frag_t<T>{};
+    }
+#pragma unroll
+    for (int ks = 0; ks < DV / 16; ++ks) {
+      vf[ks] = *reinterpret_cast<const frag_t<T>*>(kvr + DN + ks * 16 + 8 * g);
+      if (!ok) vf[ks] = frag_t<T>{};
+    }
+  }
+
+  f32x16 dk[DQK / 32], dv[DV / 32];
+#pragma unroll
+  for (int i = 0; i < DQK / 32; ++i) dk[i] = f32x16{};
+#pragma unroll
+  for (int i = 0; i < DV / 32; ++i) dv[i] = f32x16{};
+
+  const size_t hrow = (size_t)(b * H + h) * P.S_pad;
+  auto fill = [&](int stage, int qt) {
+    // rows past S are clamped to S-1 (valid memory); their P is masked to zero
+    swz_fill<T, BQ, QCPR, NW>(sQ[stage], wave, l, [&](int r) {
+      const int qi = min(qt + r, S - 1);
+      return q + ((size_t)(b * S + qi) * H + h) * DQK;
+    });
+    swz_fill<T, BQ, OCPR, NW>(sO[stage], wave, l, [&](int r) {
+      const int qi = min(qt + r, S - 1);
+      return dout + ((size_t)(b * S + qi) * H + h) * DV;
+    });
+    if (wave == NW - 1 && l < 2 * BQ / 4) {  // 8 chunks of lse2, then 8 of delta (padded rows)
+      const float* src = l < BQ / 4 ? P.lse2 + hrow + qt + 4 * l : P.delta + hrow + qt + 4 * (l - BQ / 4);
+      g2lds16(src, &sLD[stage][0]);
+    }
+  };
+
+  const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
+  fill(0, qt_begin);
+  int it = 0;
+  for (int qt = qt_begin; qt < S; qt += BQ, ++it) {
+    const int st = it & 1;
+    wait_vmem();      // this wave's part of tile `it` has landed
+    __syncthreads();  // all parts landed; everyone is done with the other stage
+    if (qt + BQ < S) fill(st ^ 1, qt + BQ);
+
+    // waves whose keys all lie after this tile's queries run it fully masked (P = 0):
+    // keeping the loop body free of per-wave branches keeps the accumulators in place
+    const bool need_mask = (P.causal && qt < k0 + 31) || (qt + BQ > S);
+    const T* tq = sQ[st];
+    const T* to = sO[st];
+
+    f32x16 sa{}, dp{};
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) mma(sa, swz_frag<T, QCPR>(tq, n, 2 * ks + g), kf[ks]);
+#pragma unroll
+    for (int ks = 0; ks < DV / 16; ++ks) mma(dp, swz_frag<T, OCPR>(to, n, 2 * ks + g), vf[ks]);
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int qrow = rr * 8 + g * 4;
+      const f32x4 lq = *reinterpret_cast<const f32x4*>(&sLD[st][qrow]);
+      const f32x4 dq = *reinterpret_cast<const f32x4*>(&sLD[st][BQ + qrow]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = rr * 4 + e;
+        float p = fast_exp2(sa[r] * P.scale_log2 - lq[e]);
+        if (need_mask) {
+          const int qi = qt + qrow + e;
+          if (qi >= S || (P.causal && my_k > qi)) p = 0.f;
+        }
+        sa[r] = p;
+        dp[r] = p * (dp[r] - dq[e]);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < BQ / 16; ++kk) {
+      const frag_t<T> pf = acc_to_frag<T>(sa, kk);
+      const frag_t<T> zf = acc_to_frag<T>(dp, kk);
+      const int ra = kk * 16 + 4 * g;
+#pragma unroll
+      for (int db = 0; db < DV / 32; ++db) mma(dv[db], swz_tr_frag<OCPR>(to, ra, ra + 8, db * 32), pf);
+#pragma unroll
+      for (int db = 0; db < DQK / 32; ++db) mma(dk[db], swz_tr_frag<QCPR>(tq, ra, ra + 8, db * 32), zf);
+    }
+  }
+
+  if (my_k >= S) return;
+  const size_t row = (size_t)(b * S + my_k) * H + h;
+  T* dkvr = (T*)P.dkv + row * DKVH;
+  T* dkvl = (T*)P.dkv_lo + row * DKVH;
+  float* dper = P.dkpe_h + row * DR;
+  auto put4 = [&](int col, float a0, float a1, float a2, float a3) {
+    bf16x4 hi = {to_elem<T>(a0), to_elem<T>(a1), to_elem<T>(a2), to_elem<T>(a3)};
+    bf16x4 lo = {to_elem<T>(a0 - to_f32(hi[0])), to_elem<T>(a1 - to_f32(hi[1])), to_elem<T>(a2 - to_f32(hi[2])),
+                 to_elem<T>(a3 - to_f32(hi[3]))};
+    *reinterpret_cast<bf16x4*>(dkvr + col) = hi;
+    *reinterpret_cast<bf16x4*>(dkvl + col) = lo;
+  };
+#pragma unroll
+  for (int db = 0; db < DQK / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int d = db * 32 + rr * 8 + g * 4;
+      const float a0 = dk[db][4 * rr] * P.scale, a1 = dk[db][4 * rr + 1] * P.scale;
+      const float a2 = dk[db][4 * rr + 2] * P.scale, a3 = dk[db][4 * rr + 3] * P.scale;
+      if (d < DN) {
+        put4(d, a0, a1, a2, a3);
+      } else {
+        f32x4 v = {a0, a1, a2, a3};
+        *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
+      }
+    }
+#pragma unroll
+  for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+      put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
+}
+
 // ------------------------------------------------------------------ dQ
 template <typename T, int DN, int DR, int DV, int BC, int WPH>
 __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
@@ -345,8 +509,8 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
         for (int e = 0; e < 8; ++e) of[ks][e] = to_elem<T>(0.f);
     }
     if (ok) {
-      lse2 = P.lse[(size_t)(b * H + h) * S + my_q] * 1.4426950408889634f;
-      dlt = P.delta[(size_t)(b * H + h) * S + my_q];
+      lse2 = P.lse2[(size_t)(b * H + h) * P.S_pad + my_q];
+      dlt = P.delta[(size_t)(b * H + h) * P.S_pad + my_q];
     }
   }
 
@@ -470,15 +634,20 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
   using Tl = BwdTiles<T>;
   BwdParams P;
   P.q = a.q; P.k_pe = a.k_pe; P.kv = a.kv; P.dout = a.dout; P.lse = a.lse; P.delta = a.delta;
+  P.lse2 = a.lse2; P.S_pad = a.S_pad;
   P.dq = a.dq; P.dkv = a.dkv; P.dkv_lo = a.dkv_lo; P.dkpe_h = a.dkpe_h;
   P.S = a.S; P.H = a.H; P.scale = a.scale; P.scale_log2 = a.scale * 1.4426950408889634f; P.causal = a.causal;
   if (stage == 0) {
     const int BS = a.B * a.S;
-    delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.delta, a.S, a.H, BS);
+    delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.lse, a.delta, a.lse2,
+                                                      a.S, a.S_pad, a.H, BS);
   } else if (stage == 1) {
     constexpr int BK = 32 * Tl::WPH_KV;
     P.n_blocks = (a.S + BK - 1) / BK;
-    dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+    if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128)
+      dkdv_ring_kernel<DN, DR, DV, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+    else
+      dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
   } else if (stage == 2) {
     constexpr int BR = 32 * Tl::WPH_Q;
     P.n_blocks = (a.S + BR - 1) / BR;

@@ -118,6 +118,76 @@ __device__ __forceinline__ void g2lds16(const void* g, void* lds) {
 // global -> LDS copies) have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+// ---------------------------------------------------------------- swizzled tiles
+// A "swizzled tile" is R rows x CPR 16-byte chunks stored without padding; logical
+// chunk c of row r lives at physical chunk c ^ swz<CPR>(r) of that row. Without
+// padding, a wave instruction of direct global->LDS loads fills 64 consecutive
+// chunks, and the XOR keeps both access patterns of the kernels free of LDS bank
+// conflicts (64 banks x 4 bytes; 16 lanes are serviced per cycle):
+//   * 16-byte row fragments: 16 lanes read one logical chunk of 16 consecutive rows;
+//   * ds_read_b64_tr_b16: a 16-lane group reads 2 adjacent chunks (c even) of 4
+//     consecutive rows starting at a multiple of 4.
+// CPR = 16 (256-byte rows): swz is a bit permutation of r & 15 whose bits 1-2 come
+//   from r & 3, so 16 consecutive rows hit 16 distinct chunks and 4 consecutive
+//   rows never share a chunk pair.
+// CPR = 24 (384-byte rows, odd rows on the other half of the banks): 3-bit swz,
+//   distinct over the 8 rows of each parity among 16 consecutive rows, and rows
+//   r, r+2 (r % 4 == 0) differ in bit 2.
+// CPR = 8 (128-byte rows, row fragments only): swz = (r >> 1) & 7.
+template <int CPR> __device__ __forceinline__ int swz(int r);
+template <> __device__ __forceinline__ int swz<16>(int r) {
+  return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+}
+template <> __device__ __forceinline__ int swz<24>(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+template <> __device__ __forceinline__ int swz<8>(int r) { return (r >> 1) & 7; }
+
+// Element offset of (row, element col) in a swizzled tile of CPR chunks per row.
+template <typename T, int CPR>
+__device__ __forceinline__ int swz_off(int row, int col) {
+  constexpr int E = 16 / sizeof(T);
+  return row * CPR * E + (((col / E) ^ swz<CPR>(row)) * E) + (col % E);
+}
+
+// 8-element row fragment (contraction along the row) at logical chunk c of `row`.
+template <typename T, int CPR>
+__device__ __forceinline__ frag_t<T> swz_frag(const T* tile, int row, int c) {
+  constexpr int E = 16 / sizeof(T);
+  return *reinterpret_cast<const frag_t<T>*>(tile + row * CPR * E + ((c ^ swz<CPR>(row)) * E));
+}
+
+// Transposing fragment from a swizzled bf16 tile: lane l gets X[ra + e][c0 + l%32]
+// (e = 0..3) and X[rb + e][c0 + l%32] (e = 0..3); see TrRead for the lane layout.
+template <int CPR>
+__device__ __forceinline__ bf16x8 swz_tr_frag(const bf16* tile, int ra, int rb, int c0) {
+  const int l = threadIdx.x & 63, s = l & 15;
+  const int col = c0 + 16 * ((l >> 4) & 1) + 4 * (s & 3);  // element column of this lane's 8 bytes
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int r0 = ra + (s >> 2), r1 = rb + (s >> 2);
+  const bf16* pa = tile + swz_off<bf16, CPR>(r0, col);
+  const bf16* pb = tile + swz_off<bf16, CPR>(r1, col);
+  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
+  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Direct global->LDS fill of a swizzled tile of NROWS x CPR chunks by NW waves:
+// wave instruction j covers physical chunks [64 j, 64 j + 64); lane i fetches the
+// logical chunk that belongs at physical chunk 64 j + i, i.e. c = p ^ swz(row), from
+// row_ptr(row) + 16 * c bytes. row_ptr must return a valid address for every row
+// (callers clamp rows past the end of the data; those rows are masked later).
+template <typename T, int NROWS, int CPR, int NW, typename RowPtr>
+__device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+  constexpr int E = 16 / sizeof(T);
+  constexpr int N = NROWS * CPR;
+  static_assert(N % 64 == 0, "tile must be whole wave instructions");
+#pragma unroll
+  for (int j = wave; j < N / 64; j += NW) {
+    const int p = j * 64 + l;
+    const int row = p / CPR, c = (p % CPR) ^ swz<CPR>(row);
+    g2lds16(row_ptr(row) + c * E, tile + j * 64 * E);
+  }
+}
+
 // Zero value of a 16-byte staging chunk.
 __device__ __forceinline__ chunk16 zero_chunk() { chunk16 z = {0, 0, 0, 0}; return z; }
 

@@ -6,6 +6,10 @@
 
 namespace laga {
 
+// Per-row backward statistics (delta, lse2) are stored with rows padded to a
+// multiple of this many queries, so query tiles can be fetched whole.
+constexpr int kRowPad = 64;
+
 // Tokens per split of the dW reduction (fixed: never depends on the head count).
 constexpr int kDwSplitTokens = 2048;
 size_t dw_split_count(int tokens);
@@ -50,7 +54,9 @@ struct AttnBwdArgs {
   const float* lse;
   void* dq;          // [B,S,H,DN+DR]
   float* dk_pe;      // [B,S,DR] fp32
-  float* delta;      // workspace [B,H,S]
+  float* delta;      // workspace [B*H][S_pad]
+  float* lse2;       // workspace [B*H][S_pad]: lse * log2(e)
+  int S_pad;         // S rounded up to kRowPad
   void* dkv;         // workspace [B,S,H,DN+DV]
   void* dkv_lo;      // workspace [B,S,H,DN+DV], bf16 only: dKV - bf16(dKV) rounded to bf16
   float* dkpe_h;     // workspace [B,S,H,DR]
