@@ -19,7 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblaga.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_bwd.hip"]
+SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -32,9 +32,17 @@ FLAGS = [
 ]
 
 
+# Per-file code-generation choices (measured: with MFMA results kept in VGPRs the
+# softmax / dZ arithmetic on the accumulators needs no AGPR<->VGPR copies).
+EXTRA = {
+    "attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stderr}")

@@ -23,44 +23,13 @@
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
 #include "common.hpp"
 #include "kernels.hpp"
+#include "bwd_common.hpp"
 
 namespace laga {
 
+using namespace bwd;
+
 namespace {
-
-// LDS row pitch (elements) of a tile read both with 16-byte row fragments and
-// with transposing reads: for 16-bit types the pitch in dwords is chosen
-// = 12, 28, 36 or 52 (mod 64) so that neither access pattern has bank
-// conflicts; fp32 rows are padded to stay 32-byte aligned.
-template <typename T>
-constexpr int lds_pitch(int cols) {
-  if (sizeof(T) == 4) return cols + 8;
-  for (int pad = 8; pad < 136; pad += 16) {
-    const int dw = ((cols + pad) / 2) % 64;
-    if (dw == 12 || dw == 28 || dw == 36 || dw == 52) return cols + pad;
-  }
-  return cols + 8;
-}
-
-constexpr int round32(int x) { return (x + 31) / 32 * 32; }
-
-struct BwdParams {
-  const void* q;
-  const void* k_pe;
-  const void* kv;
-  const void* dout;
-  const float* lse;
-  const float* delta;  // [B*H][S_pad]
-  const float* lse2;   // [B*H][S_pad], lse * log2(e)
-  int S_pad;
-  void* dq;
-  void* dkv;       // [B,S,H,DN+DV] element dtype
-  void* dkv_lo;    // [B,S,H,DN+DV] bf16 low halves (bf16 only; else unused)
-  float* dkpe_h;   // [B,S,H,DR] fp32
-  int S, H, n_blocks;
-  float scale, scale_log2;
-  int causal;
-};
 
 // delta[b,h,t] = sum_e dout[b,t,h,e] * out[b,t,h,e]. One wave per token: the token's
 // [H, DV] rows of out and dout are contiguous, lanes read consecutive 16-byte chunks,
@@ -306,15 +275,16 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 // the per-row lse2 / delta) stream through a two-stage LDS ring filled by direct
 // global->LDS loads into swizzled, unpadded tiles, so no registers are spent on
 // staging and one barrier per tile suffices. Math as in dkdv_kernel.
-template <int DN, int DR, int DV, int WPH>
+template <int DN, int DR, int DV, int WPH, int NS>
 __global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 32 * WPH;
   constexpr int QCPR = DQK / 8, OCPR = DV / 8;  // 16-byte chunks per row
   static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
-  __shared__ __attribute__((aligned(16))) T sQ[2][BQ * DQK];
-  __shared__ __attribute__((aligned(16))) T sO[2][BQ * DV];
-  __shared__ __attribute__((aligned(16))) float sLD[2][2 * BQ];  // lse2 then delta
+  __shared__ __attribute__((aligned(16))) T sQ[NS][BQ * DQK];
+  __shared__ __attribute__((aligned(16))) T sO[NS][BQ * DV];
+  __shared__ __attribute__((aligned(16))) float sLD[NS][2 * BQ];  // lse2 then delta
+  constexpr int F = (BQ * (QCPR + OCPR) / 64) / NW;  // load instructions per wave per tile (at least)
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -374,13 +344,13 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
   };
 
   const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
-  fill(0, qt_begin);
-  int it = 0;
-  for (int qt = qt_begin; qt < S; qt += BQ, ++it) {
-    const int st = it & 1;
-    wait_vmem();      // this wave's part of tile `it` has landed
-    __syncthreads();  // all parts landed; everyone is done with the other stage
-    if (qt + BQ < S) fill(st ^ 1, qt + BQ);
+  const int ntiles = (S - qt_begin + BQ - 1) / BQ;
+  for (int t = 0; t < NS - 1 && t < ntiles; ++t) fill(t, qt_begin + t * BQ);
+  for (int it = 0; it < ntiles; ++it) {
+    const int qt = qt_begin + it * BQ, st = it % NS;
+    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));
+    __syncthreads();  // tile `it` has landed for all waves; stage (it - 1) % NS is free
+    if (it + NS - 1 < ntiles) fill((it + NS - 1) % NS, qt_begin + (it + NS - 1) * BQ);
 
     // waves whose keys all lie after this tile's queries run it fully masked (P = 0):
     // keeping the loop body free of per-wave branches keeps the accumulators in place
@@ -455,161 +425,6 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
       put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
 }
 
-// ------------------------------------------------------------------ dQ
-template <typename T, int DN, int DR, int DV, int BC, int WPH>
-__global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
-  constexpr int DQK = DN + DR, DKVH = DN + DV, DQK32 = round32(DQK);
-  constexpr int NT = 64 * WPH, BR = 32 * WPH, E = Elems16<T>::n;
-  constexpr int PK = lds_pitch<T>(DQK32), PV = lds_pitch<T>(DV);
-  constexpr int KCH = DQK / E, VCH = DV / E;
-  constexpr int TILE_CHUNKS = BC * (KCH + VCH);
-  constexpr int PER_THREAD = (TILE_CHUNKS + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) T sK[BC * PK];
-  __shared__ __attribute__((aligned(16))) T sV[BC * PV];
-
-  const T* __restrict__ q = (const T*)P.q;
-  const T* __restrict__ kpe = (const T*)P.k_pe;
-  const T* __restrict__ kv = (const T*)P.kv;
-  const T* __restrict__ dout = (const T*)P.dout;
-  const int S = P.S, H = P.H;
-
-  const int total = P.n_blocks * H * gridDim.y;
-  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
-  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;  // heavy first
-  const int bh = lin / P.n_blocks;
-  const int b = bh / H, h = bh % H;
-
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
-  const int q0 = qblk * BR + wave * 32;
-  const int my_q = q0 + n;
-  const int wg_qend = min(S, (qblk + 1) * BR);
-  const int kend = P.causal ? wg_qend : S;
-
-  if (DQK32 > DQK)
-    for (int i = tid; i < BC * (DQK32 - DQK); i += NT)
-      sK[(i / (DQK32 - DQK)) * PK + DQK + i % (DQK32 - DQK)] = to_elem<T>(0.f);
-
-  frag_t<T> qf[DQK / 16], of[DV / 16];
-  float lse2 = 0.f, dlt = 0.f;
-  {
-    const bool ok = my_q < S;
-    const size_t base = (size_t)(b * S + (ok ? my_q : 0)) * H + h;
-#pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) {
-      if (ok) qf[ks] = *reinterpret_cast<const frag_t<T>*>(q + base * DQK + ks * 16 + 8 * g);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qf[ks][e] = to_elem<T>(0.f);
-    }
-#pragma unroll
-    for (int ks = 0; ks < DV / 16; ++ks) {
-      if (ok) of[ks] = *reinterpret_cast<const frag_t<T>*>(dout + base * DV + ks * 16 + 8 * g);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) of[ks][e] = to_elem<T>(0.f);
-    }
-    if (ok) {
-      lse2 = P.lse2[(size_t)(b * H + h) * P.S_pad + my_q];
-      dlt = P.delta[(size_t)(b * H + h) * P.S_pad + my_q];
-    }
-  }
-
-  f32x16 dqa[DQK32 / 32];
-#pragma unroll
-  for (int i = 0; i < DQK32 / 32; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dqa[i][r] = 0.f;
-
-  chunk16 stage[PER_THREAD];
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * NT;
-      stage[i] = zero_chunk();
-      if (c < TILE_CHUNKS) {
-        const int row = c / (KCH + VCH), j = c % (KCH + VCH);
-        const int key = kt + row;
-        if (key < S) {
-          const size_t r = (size_t)(b * S + key);
-          const T* src = j < DN / E ? kv + (r * H + h) * DKVH + j * E
-                       : j < KCH    ? kpe + r * DR + (j - DN / E) * E
-                                    : kv + (r * H + h) * DKVH + DN + (j - KCH) * E;
-          stage[i] = *reinterpret_cast<const chunk16*>(src);
-        }
-      }
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * NT;
-      if (c < TILE_CHUNKS) {
-        const int row = c / (KCH + VCH), j = c % (KCH + VCH);
-        T* dst = j < KCH ? sK + row * PK + j * E : sV + row * PV + (j - KCH) * E;
-        *reinterpret_cast<chunk16*>(dst) = stage[i];
-      }
-    }
-  };
-
-  load_tile(0);
-  for (int kt = 0; kt < kend; kt += BC) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + BC < kend) load_tile(kt + BC);
-
-    const bool active = q0 < S && (!P.causal || kt <= q0 + 31);
-    if (!active) continue;
-    const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
-
-    f32x16 sa[BC / 32], dp[BC / 32];
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { sa[kb][r] = 0.f; dp[kb][r] = 0.f; }
-#pragma unroll
-      for (int ks = 0; ks < DQK / 16; ++ks)
-        mma(sa[kb], lds_frag<T>(sK + (kb * 32 + n) * PK + ks * 16 + 8 * g), qf[ks]);
-#pragma unroll
-      for (int ks = 0; ks < DV / 16; ++ks)
-        mma(dp[kb], lds_frag<T>(sV + (kb * 32 + n) * PV + ks * 16 + 8 * g), of[ks]);
-    }
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float p = fast_exp2(sa[kb][r] * P.scale_log2 - lse2);
-        if (need_mask) {
-          const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (key >= S || (P.causal && key > my_q)) p = 0.f;
-        }
-        dp[kb][r] = p * (dp[kb][r] - dlt);
-      }
-#pragma unroll
-    for (int kk = 0; kk < BC / 16; ++kk) {
-      const frag_t<T> zf = acc_to_frag<T>(dp[kk >> 1], kk & 1);
-      const int ra = kk * 16 + 4 * g;
-#pragma unroll
-      for (int db = 0; db < DQK32 / 32; ++db) mma(dqa[db], TrRead<T>::get(sK, PK, ra, ra + 8, db * 32), zf);
-    }
-  }
-
-  if (my_q >= S) return;
-  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
-#pragma unroll
-  for (int db = 0; db < DQK32 / 32; ++db)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int d = db * 32 + rr * 8 + g * 4;
-      if (d < DQK) {
-        typename FragOf<T>::half v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
-        *reinterpret_cast<typename FragOf<T>::half*>(dqr + d) = v;
-      }
-    }
-}
-
 // dk_pe[b,t,:] = sum_{h ascending} dkpe_h[b,t,h,:]   (one thread per 4 outputs, fp32)
 template <int DR>
 __global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ part, float* __restrict__ dkpe, int H,
@@ -622,10 +437,6 @@ __global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ par
   for (int h = 1; h < H; ++h) s += *reinterpret_cast<const f32x4*>(src + (size_t)h * DR);
   *reinterpret_cast<f32x4*>(dkpe + (size_t)bt * DR + c) = s;
 }
-
-template <typename T> struct BwdTiles;
-template <> struct BwdTiles<bf16> { static constexpr int BQ = 32, BC = 64, WPH_KV = 4, WPH_Q = 4; };
-template <> struct BwdTiles<float> { static constexpr int BQ = 32, BC = 32, WPH_KV = 4, WPH_Q = 4; };
 
 }  // namespace
 
@@ -645,13 +456,11 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
     constexpr int BK = 32 * Tl::WPH_KV;
     P.n_blocks = (a.S + BK - 1) / BK;
     if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128)
-      dkdv_ring_kernel<DN, DR, DV, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+      dkdv_ring_kernel<DN, DR, DV, Tl::WPH_KV, 4><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
     else
       dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
   } else if (stage == 2) {
-    constexpr int BR = 32 * Tl::WPH_Q;
-    P.n_blocks = (a.S + BR - 1) / BR;
-    dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_Q, 0, st>>>(P);
+    return launch_bwd_dq<T, DN, DR, DV>(P, a.B, st);
   } else {
     const int n4 = a.B * a.S * DR / 4;
     dkpe_kernel<DR><<<(n4 + 255) / 256, 256, 0, st>>>(a.dkpe_h, a.dk_pe, a.H, n4);

@@ -81,23 +81,27 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
     }
   }
 
-  // scale (base 2) and mask; only tiles crossing the diagonal or the end need the mask
+  // mask (only tiles crossing the diagonal or the end), running max on the raw scores
+  // (scale > 0), p = exp2(s * scale_log2 - m) as one FMA + v_exp_f32, O rescaled only
+  // when some lane's max moved: the same arithmetic, in the same order, as the ring
+  // kernel, so the two forward kernels agree bit for bit
   const bool need_mask = (causal && kt + BC - 1 > q0) || (kt + BC > S);
-  float mloc = -INFINITY;
+  if (need_mask) {
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        if (key >= S || (causal && key > my_q)) sacc[kb][r] = -INFINITY;
+      }
+  }
+  float mraw = -INFINITY;
 #pragma unroll
   for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float s = sacc[kb][r] * scale_log2;
-      if (need_mask) {
-        const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        if (key >= S || (causal && key > my_q)) s = -INFINITY;
-      }
-      sacc[kb][r] = s;
-      mloc = fmaxf(mloc, s);
-    }
-  mloc = wave_xor32_max(mloc);
-  const float m_new = fmaxf(m, mloc);
+    for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[kb][r]);
+  mraw = wave_xor32_max(mraw);
+  const float m_new = fmaxf(m, mraw * scale_log2);
   const float m_use = m_new == -INFINITY ? 0.f : m_new;
   const float alpha = fast_exp2(m - m_use);
   float ps = 0.f;
@@ -105,16 +109,16 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
   for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float p = fast_exp2(sacc[kb][r] - m_use);
+      const float p = fast_exp2(__builtin_fmaf(sacc[kb][r], scale_log2, -m_use));
       sacc[kb][r] = p;
       ps += p;
     }
   lsum = lsum * alpha + ps;
   m = m_new;
+  if (__ballot(alpha != 1.f)) {
 #pragma unroll
-  for (int i = 0; i < DV / 32; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+    for (int i = 0; i < DV / 32; ++i) oacc[i] *= alpha;
+  }
 
   frag_t<T> pf[BC / 16];
 #pragma unroll
@@ -253,6 +257,153 @@ void attn_fwd_kernel(FwdParams P) {
   if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
 }
 
+
+// ------------------------------------------------------------------ ring variant
+// bf16 forward for 128-wide K_nope / V and 64-wide k_pe. Key tiles stream through a
+// two-stage LDS ring filled by direct global->LDS loads into swizzled, unpadded
+// tiles (no staging registers, one barrier per tile). There is no per-wave branch
+// around the MFMAs: a wave whose queries all precede a tile runs it fully masked
+// (p = 0, m and O unchanged). Softmax details: the running max is taken on the raw
+// scores (scale > 0), p = exp2(s * scale_log2 - m) is one FMA and one v_exp_f32,
+// and O^T is rescaled only when some lane's running max moved.
+template <int DN, int DR, int DV, int BC, int WPH, int NS>
+__global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, BR = 32 * WPH;
+  constexpr int KCPR = DN / 8, PCPR = DR / 8, VCPR = DV / 8;
+  static_assert(KCPR == 16 && PCPR == 8 && VCPR == 16, "swizzles are defined for 128/64/128-wide rows");
+  __shared__ __attribute__((aligned(16))) T sK[NS][BC * DN];
+  __shared__ __attribute__((aligned(16))) T sP[NS][BC * DR];
+  __shared__ __attribute__((aligned(16))) T sV[NS][BC * DV];
+  constexpr int F = (BC * (KCPR + VCPR + PCPR) / 64) / NW;  // load instructions per wave per tile
+
+  const T* __restrict__ q = (const T*)P.q;
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ kv = (const T*)P.kv;
+  const int S = P.S, H = P.H;
+
+  const int total = P.n_qblocks * P.n_hgroups * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int qb = P.n_qblocks - 1 - lin % P.n_qblocks;
+  const int bh = lin / P.n_qblocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
+  const int q0 = qb * BR + wave * 32;
+  const int my_q = q0 + n;
+  const int kend = P.causal ? min(S, (qb + 1) * BR) : S;
+
+  frag_t<T> qf[DQK / 16];
+  {
+    const bool ok = my_q < S;
+    const T* qrow = q + ((size_t)(b * S + (ok ? my_q : 0)) * H + h) * DQK;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      qf[ks] = *reinterpret_cast<const frag_t<T>*>(qrow + ks * 16 + 8 * g);
+      if (!ok) qf[ks] = frag_t<T>{};
+    }
+  }
+  f32x16 oacc[DV / 32];
+#pragma unroll
+  for (int i = 0; i < DV / 32; ++i) oacc[i] = f32x16{};
+  float m = -INFINITY, lsum = 0.f;
+
+  auto fill = [&](int stage, int kt) {
+    // key rows past S are clamped to S-1 (valid memory) and masked below
+    swz_fill<T, BC, KCPR, NW>(sK[stage], wave, l, [&](int r) {
+      return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH;
+    });
+    swz_fill<T, BC, VCPR, NW>(sV[stage], wave, l, [&](int r) {
+      return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH + DN;
+    });
+    swz_fill<T, BC, PCPR, NW>(sP[stage], wave, l, [&](int r) {
+      return kpe + (size_t)(b * S + min(kt + r, S - 1)) * DR;
+    });
+  };
+
+  const int ntiles = (kend + BC - 1) / BC;
+  for (int t = 0; t < NS - 1 && t < ntiles; ++t) fill(t, t * BC);
+  for (int it = 0; it < ntiles; ++it) {
+    const int kt = it * BC, st = it % NS;
+    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));
+    __syncthreads();  // tile `it` has landed for all waves; stage (it - 1) % NS is free
+    if (it + NS - 1 < ntiles) fill((it + NS - 1) % NS, (it + NS - 1) * BC);
+    const T* tk = sK[st];
+    const T* tp = sP[st];
+    const T* tv = sV[st];
+
+    f32x16 sacc[BC / 32];
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb) {
+      sacc[kb] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < DQK / 16; ++ks) {
+        const frag_t<T> a = ks < DN / 16 ? swz_frag<T, KCPR>(tk, kb * 32 + n, 2 * ks + g)
+                                         : swz_frag<T, PCPR>(tp, kb * 32 + n, 2 * (ks - DN / 16) + g);
+        mma(sacc[kb], a, qf[ks]);
+      }
+    }
+    const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
+    if (need_mask) {
+#pragma unroll
+      for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          if (key >= S || (P.causal && key > my_q)) sacc[kb][r] = -INFINITY;
+        }
+    }
+    float mraw = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[kb][r]);
+    mraw = wave_xor32_max(mraw);
+    const float m_new = fmaxf(m, mraw * P.scale_log2);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = fast_exp2(m - m_use);
+    float ps = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(__builtin_fmaf(sacc[kb][r], P.scale_log2, -m_use));
+        sacc[kb][r] = p;
+        ps += p;
+      }
+    lsum = lsum * alpha + ps;
+    m = m_new;
+    if (__ballot(alpha != 1.f)) {
+#pragma unroll
+      for (int i = 0; i < DV / 32; ++i) oacc[i] *= alpha;
+    }
+    frag_t<T> pf[BC / 16];
+#pragma unroll
+    for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
+#pragma unroll
+    for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+      for (int kk = 0; kk < BC / 16; ++kk) {
+        const int ra = kk * 16 + 4 * g;
+        mma(oacc[db], swz_tr_frag<VCPR>(tv, ra, ra + 8, db * 32), pf[kk]);
+      }
+  }
+
+  if (my_q >= S) return;
+  const float ltot = wave_xor32_sum(lsum);
+  const float inv = 1.f / ltot;
+  T* orow = (T*)P.out + ((size_t)(b * S + my_q) * H + h) * DV;
+#pragma unroll
+  for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      bf16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(oacc[db][4 * rr + e] * inv);
+      *reinterpret_cast<bf16x4*>(orow + db * 32 + rr * 8 + g * 4) = v;
+    }
+  if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
+}
 
 // ------------------------------------------------------------------ fused variant
 // No per-head K/V tensor exists in HBM. For each key tile the latent rows
@@ -474,8 +625,12 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   P.scale_log2 = a.scale * 1.4426950408889634f;
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * P.n_hgroups, a.B, 1);
-  using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
-  attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);
+  if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128 && Tl::G == 1) {
+    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, Tl::WPH, 2><<<grid, 64 * Tl::WPH, 0, st>>>(P);
+  } else {
+    using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
+    attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);
+  }
   return hipGetLastError();
 }
 

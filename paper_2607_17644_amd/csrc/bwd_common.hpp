@@ -1,0 +1,48 @@
+// Declarations shared by the backward kernels (attn_bwd.hip, attn_bwd_dq.hip).
+#pragma once
+#include "common.hpp"
+
+namespace laga {
+namespace bwd {
+
+// LDS row pitch (elements) of a tile read both with 16-byte row fragments and
+// with transposing reads: for 16-bit types the pitch in dwords is chosen
+// = 12, 28, 36 or 52 (mod 64) so that neither access pattern has bank
+// conflicts; fp32 rows are padded to stay 32-byte aligned.
+template <typename T>
+constexpr int lds_pitch(int cols) {
+  if (sizeof(T) == 4) return cols + 8;
+  for (int pad = 8; pad < 136; pad += 16) {
+    const int dw = ((cols + pad) / 2) % 64;
+    if (dw == 12 || dw == 28 || dw == 36 || dw == 52) return cols + pad;
+  }
+  return cols + 8;
+}
+
+constexpr int round32(int x) { return (x + 31) / 32 * 32; }
+
+struct BwdParams {
+  const void* q;
+  const void* k_pe;
+  const void* kv;
+  const void* dout;
+  const float* lse;
+  const float* delta;  // [B*H][S_pad]
+  const float* lse2;   // [B*H][S_pad], lse * log2(e)
+  int S_pad;
+  void* dq;
+  void* dkv;       // [B,S,H,DN+DV] element dtype
+  void* dkv_lo;    // [B,S,H,DN+DV] bf16 low halves (bf16 only; else unused)
+  float* dkpe_h;   // [B,S,H,DR] fp32
+  int S, H, n_blocks;
+  float scale, scale_log2;
+  int causal;
+};
+
+template <typename T> struct BwdTiles;
+template <> struct BwdTiles<bf16> { static constexpr int BQ = 32, BC = 64, WPH_KV = 4, WPH_Q = 4; };
+template <> struct BwdTiles<float> { static constexpr int BQ = 32, BC = 32, WPH_KV = 4, WPH_Q = 4; };
+
+
+}  // namespace bwd
+}  // namespace laga

@@ -118,6 +118,28 @@ __device__ __forceinline__ void g2lds16(const void* g, void* lds) {
 // global -> LDS copies) have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Wait until at most N of this wave's vector-memory loads are outstanding (loads
+// complete in issue order, so everything issued before the last N has landed).
+// s_waitcnt immediate on gfx9: vmcnt in bits [3:0] and [15:14], expcnt [6:4] and
+// lgkmcnt [11:8] left at their maxima (no wait on them).
+template <int N>
+__device__ __forceinline__ void wait_vmem_le() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Ring of NS LDS stages fed by direct loads, at least F load instructions per wave
+// per tile: before consuming a tile, wait until only the `ahead` tiles issued after
+// it (ahead <= NS - 2) can still be in flight; with fewer tiles ahead (the end of
+// the sweep) wait for everything.
+template <int NS, int F>
+__device__ __forceinline__ void ring_wait(int ahead) {
+  static_assert(NS >= 2 && NS <= 4, "ring depth");
+  if (NS >= 4 && ahead >= 2) wait_vmem_le<F * 2>();
+  else if (NS >= 3 && ahead >= 1) wait_vmem_le<F>();
+  else wait_vmem();
+}
+
 // ---------------------------------------------------------------- swizzled tiles
 // A "swizzled tile" is R rows x CPR 16-byte chunks stored without padding; logical
 // chunk c of row r lives at physical chunk c ^ swz<CPR>(r) of that row. Without
@@ -133,13 +155,13 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 // CPR = 24 (384-byte rows, odd rows on the other half of the banks): 3-bit swz,
 //   distinct over the 8 rows of each parity among 16 consecutive rows, and rows
 //   r, r+2 (r % 4 == 0) differ in bit 2.
-// CPR = 8 (128-byte rows, row fragments only): swz = (r >> 1) & 7.
+// CPR = 8 (128-byte rows, rows of equal parity share bank halves): the CPR = 24 rule.
 template <int CPR> __device__ __forceinline__ int swz(int r);
 template <> __device__ __forceinline__ int swz<16>(int r) {
   return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
 }
 template <> __device__ __forceinline__ int swz<24>(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
-template <> __device__ __forceinline__ int swz<8>(int r) { return (r >> 1) & 7; }
+template <> __device__ __forceinline__ int swz<8>(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
 
 // Element offset of (row, element col) in a swizzled tile of CPR chunks per row.
 template <typename T, int CPR>
@@ -173,10 +195,11 @@ __device__ __forceinline__ bf16x8 swz_tr_frag(const bf16* tile, int ra, int rb, 
 // Direct global->LDS fill of a swizzled tile of NROWS x CPR chunks by NW waves:
 // wave instruction j covers physical chunks [64 j, 64 j + 64); lane i fetches the
 // logical chunk that belongs at physical chunk 64 j + i, i.e. c = p ^ swz(row), from
-// row_ptr(row) + 16 * c bytes. row_ptr must return a valid address for every row
-// (callers clamp rows past the end of the data; those rows are masked later).
-template <typename T, int NROWS, int CPR, int NW, typename RowPtr>
-__device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+// chunk_ptr(row, c) (the address of that chunk's first element). chunk_ptr must
+// return a valid address for every row (callers clamp rows past the end of the
+// data; those rows are masked later).
+template <typename T, int NROWS, int CPR, int NW, typename ChunkPtr>
+__device__ __forceinline__ void swz_fill_chunks(T* tile, int wave, int l, ChunkPtr chunk_ptr) {
   constexpr int E = 16 / sizeof(T);
   constexpr int N = NROWS * CPR;
   static_assert(N % 64 == 0, "tile must be whole wave instructions");
@@ -184,8 +207,15 @@ __device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_pt
   for (int j = wave; j < N / 64; j += NW) {
     const int p = j * 64 + l;
     const int row = p / CPR, c = (p % CPR) ^ swz<CPR>(row);
-    g2lds16(row_ptr(row) + c * E, tile + j * 64 * E);
+    g2lds16(chunk_ptr(row, c), tile + j * 64 * E);
   }
+}
+
+// Same, for tiles whose rows are contiguous in global memory: row_ptr(row) + 16 * c bytes.
+template <typename T, int NROWS, int CPR, int NW, typename RowPtr>
+__device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+  constexpr int E = 16 / sizeof(T);
+  swz_fill_chunks<T, NROWS, CPR, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
 }
 
 // Zero value of a 16-byte staging chunk.
