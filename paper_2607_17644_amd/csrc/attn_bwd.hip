@@ -21,6 +21,8 @@
 //                  transposing LDS reads; it recomputes S and dP (the price of
 //                  not accumulating dQ with atomics)
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "bwd_common.hpp"
@@ -425,6 +427,168 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
       put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
 }
 
+// Key-stationary backward with 16 keys per wave on the 16x16x32 MFMA: the per-wave
+// state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
+// the 32-key layout, so two waves share each SIMD and hide each other's latencies.
+// A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
+// stream through an NS-stage LDS ring (direct global->LDS loads, swizzled tiles).
+//   S = Q K^T, dP = dO V^T: A = Q / dO rows (16-byte row fragments), B = the lane's
+//       key / value row; accumulator: lane <-> key, 4 queries per 16-query block.
+//   dV^T += dO^T P, dK^T += Q^T dZ: the contraction over the tile's 32 queries takes
+//       P / dZ straight from the accumulators in the order {4G..4G+3, 16+4G..16+4G+3}
+//       (G = lane / 16), matched by two transposing 4-row reads of dO / Q.
+template <int DN, int DR, int DV, int WPH>
+__global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 16 * WPH;
+  constexpr int QCPR = DQK / 8, OCPR = DV / 8;
+  static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
+  // two ring stages as distinct LDS objects (so the compiler does not make the reads
+  // of one stage wait for the direct loads into the other)
+  __shared__ __attribute__((aligned(16))) T sQ0[BQ * DQK], sQ1[BQ * DQK];
+  __shared__ __attribute__((aligned(16))) T sO0[BQ * DV], sO1[BQ * DV];
+  __shared__ __attribute__((aligned(16))) float sLD0[2 * BQ], sLD1[2 * BQ];  // lse2 then delta
+
+  const T* __restrict__ q = (const T*)P.q;
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ kv = (const T*)P.kv;
+  const T* __restrict__ dout = (const T*)P.dout;
+  const int S = P.S, H = P.H;
+
+  const int total = P.n_blocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int kb = lin % P.n_blocks;
+  const int bh = lin / P.n_blocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, j = l & 15, G = l >> 4;
+  const int k0 = kb * BK + wave * 16;
+  const int my_k = k0 + j;
+
+  bf16x8 kf[DQK / 32], vf[DV / 32];
+  {
+    const bool ok = my_k < S;
+    const size_t row = (size_t)(b * S + (ok ? my_k : 0));
+    const T* kvr = kv + (row * H + h) * DKVH;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 32; ++ks) {
+      const int d = ks * 32 + G * 8;
+      const T* src = d < DN ? kvr + d : kpe + row * DR + (d - DN);
+      kf[ks] = *reinterpret_cast<const bf16x8*>(src);
+      if (!ok) kf[ks] = bf16x8{};
+    }
+#pragma unroll
+    for (int ks = 0; ks < DV / 32; ++ks) {
+      vf[ks] = *reinterpret_cast<const bf16x8*>(kvr + DN + ks * 32 + G * 8);
+      if (!ok) vf[ks] = bf16x8{};
+    }
+  }
+
+  f32x4 dk[DQK / 16], dv[DV / 16];
+#pragma unroll
+  for (int i = 0; i < DQK / 16; ++i) dk[i] = f32x4{};
+#pragma unroll
+  for (int i = 0; i < DV / 16; ++i) dv[i] = f32x4{};
+
+  const size_t hrow = (size_t)(b * H + h) * P.S_pad;
+  auto fill = [&](T* dq_, T* do_, float* dld, int qt) {
+    swz_fill<T, BQ, QCPR, NW>(dq_, wave, l, [&](int r) {
+      return q + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DQK;
+    });
+    swz_fill<T, BQ, OCPR, NW>(do_, wave, l, [&](int r) {
+      return dout + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DV;
+    });
+    if (wave == NW - 1 && l < 2 * BQ / 4) {
+      const float* src = l < BQ / 4 ? P.lse2 + hrow + qt + 4 * l : P.delta + hrow + qt + 4 * (l - BQ / 4);
+      g2lds16(src, dld);
+    }
+  };
+
+  const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
+  const int ntiles = (S - qt_begin + BQ - 1) / BQ;
+  fill(sQ0, sO0, sLD0, qt_begin);
+  auto step = [&](auto stage, int it) {
+    constexpr int ST = decltype(stage)::value;
+    const int qt = qt_begin + it * BQ;
+    wait_vmem();      // this wave's loads of tile `it` have landed
+    __syncthreads();  // ... and everyone's; the other stage is free
+    if (it + 1 < ntiles) {
+      if constexpr (ST == 0) fill(sQ1, sO1, sLD1, qt + BQ);
+      else fill(sQ0, sO0, sLD0, qt + BQ);
+    }
+    const T* tq = ST == 0 ? sQ0 : sQ1;
+    const T* to = ST == 0 ? sO0 : sO1;
+    const float* tld = ST == 0 ? sLD0 : sLD1;
+    const bool need_mask = (P.causal && qt < k0 + 15) || (qt + BQ > S);
+
+    f32x4 sa[2], dp[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      sa[qb] = f32x4{};
+      dp[qb] = f32x4{};
+#pragma unroll
+      for (int ks = 0; ks < DQK / 32; ++ks) mma16(sa[qb], swz_frag<T, QCPR>(tq, qb * 16 + j, 4 * ks + G), kf[ks]);
+#pragma unroll
+      for (int ks = 0; ks < DV / 32; ++ks) mma16(dp[qb], swz_frag<T, OCPR>(to, qb * 16 + j, 4 * ks + G), vf[ks]);
+    }
+    bf16x8 pf, zf;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qrow = qb * 16 + G * 4;
+      const f32x4 lq = *reinterpret_cast<const f32x4*>(tld + qrow);
+      const f32x4 dq = *reinterpret_cast<const f32x4*>(tld + BQ + qrow);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float p = fast_exp2(__builtin_fmaf(sa[qb][e], P.scale_log2, -lq[e]));
+        if (need_mask) {
+          const int qi = qt + qrow + e;
+          if (qi >= S || (P.causal && my_k > qi)) p = 0.f;
+        }
+        pf[qb * 4 + e] = to_elem<T>(p);
+        zf[qb * 4 + e] = to_elem<T>(p * (dp[qb][e] - dq[e]));
+      }
+    }
+    const int ra = 4 * G, rb = 16 + 4 * G;
+#pragma unroll
+    for (int db = 0; db < DV / 16; ++db) mma16(dv[db], swz_tr_frag16<OCPR>(to, ra, rb, db * 16), pf);
+#pragma unroll
+    for (int db = 0; db < DQK / 16; ++db) mma16(dk[db], swz_tr_frag16<QCPR>(tq, ra, rb, db * 16), zf);
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+  }
+
+  if (my_k >= S) return;
+  const size_t row = (size_t)(b * S + my_k) * H + h;
+  T* dkvr = (T*)P.dkv + row * DKVH;
+  T* dkvl = (T*)P.dkv_lo + row * DKVH;
+  float* dper = P.dkpe_h + row * DR;
+  auto put4 = [&](int col, const f32x4& a, float sc) {
+    bf16x4 hi, lo;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = a[e] * sc;
+      hi[e] = to_elem<T>(x);
+      lo[e] = to_elem<T>(x - to_f32(hi[e]));
+    }
+    *reinterpret_cast<bf16x4*>(dkvr + col) = hi;
+    *reinterpret_cast<bf16x4*>(dkvl + col) = lo;
+  };
+#pragma unroll
+  for (int db = 0; db < DQK / 16; ++db) {
+    const int d = db * 16 + G * 4;
+    if (d < DN) {
+      put4(d, dk[db], P.scale);
+    } else {
+      f32x4 v = dk[db] * P.scale;
+      *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
+    }
+  }
+#pragma unroll
+  for (int db = 0; db < DV / 16; ++db) put4(DN + db * 16 + G * 4, dv[db], 1.f);
+}
+
 // dk_pe[b,t,:] = sum_{h ascending} dkpe_h[b,t,h,:]   (one thread per 4 outputs, fp32)
 template <int DR>
 __global__ __launch_bounds__(256) void dkpe_kernel(const float* __restrict__ part, float* __restrict__ dkpe, int H,
@@ -453,12 +617,15 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
     delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.lse, a.delta, a.lse2,
                                                       a.S, a.S_pad, a.H, BS);
   } else if (stage == 1) {
-    constexpr int BK = 32 * Tl::WPH_KV;
-    P.n_blocks = (a.S + BK - 1) / BK;
-    if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128)
-      dkdv_ring_kernel<DN, DR, DV, Tl::WPH_KV, 4><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
-    else
+    if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
+      constexpr int WPH16 = 8, BK = 16 * WPH16;
+      P.n_blocks = (a.S + BK - 1) / BK;
+      dkdv16_kernel<DN, DR, DV, WPH16><<<dim3(P.n_blocks * a.H, a.B), 64 * WPH16, 0, st>>>(P);
+    } else {
+      constexpr int BK = 32 * Tl::WPH_KV;
+      P.n_blocks = (a.S + BK - 1) / BK;
       dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+    }
   } else if (stage == 2) {
     return launch_bwd_dq<T, DN, DR, DV>(P, a.B, st);
   } else {

@@ -1,6 +1,8 @@
 // Query-stationary dQ pass of the attention backward (gfx950); see attn_bwd.hip for
 // the whole backward. Built with MFMA results kept in VGPRs (the dZ arithmetic on
 // the dP accumulators then needs no AGPR<->VGPR copies).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "bwd_common.hpp"
@@ -171,18 +173,19 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
 // as one 192-wide swizzled tile, V as a 128-wide one) stream through a two-stage
 // LDS ring of direct global->LDS loads; one barrier per tile; no per-wave branch
 // around the MFMAs (tiles entirely after a wave's queries run fully masked).
-template <int DN, int DR, int DV, int BC, int WPH, int NS>
+template <int DN, int DR, int DV, int BC, int WPH>
 __global__ __launch_bounds__(64 * WPH, 2) void dq_ring_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, BR = 32 * WPH;
   constexpr int KCPR = DQK / 8, VCPR = DV / 8, NCPR = DN / 8;
   static_assert(KCPR == 24 && VCPR == 16, "swizzles are defined for 192/128-wide rows");
-  __shared__ __attribute__((aligned(16))) T sK[NS][BC * DQK];
-  __shared__ __attribute__((aligned(16))) T sV[NS][BC * DV];
+  // two ring stages as distinct LDS objects (so the compiler does not make the reads
+  // of one stage wait for the direct loads into the other)
+  __shared__ __attribute__((aligned(16))) T sK0[BC * DQK], sK1[BC * DQK];
+  __shared__ __attribute__((aligned(16))) T sV0[BC * DV], sV1[BC * DV];
   // the workgroup's dO rows stay in LDS (B operand of dP^T = V dO^T), which keeps
   // the per-lane state small enough for two waves per SIMD
   __shared__ __attribute__((aligned(16))) T sDO[BR * DV];
-  constexpr int F = (BC * (KCPR + VCPR) / 64) / NW;  // load instructions per wave per tile
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -224,25 +227,29 @@ __global__ __launch_bounds__(64 * WPH, 2) void dq_ring_kernel(BwdParams P) {
 #pragma unroll
   for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
 
-  auto fill = [&](int stage, int kt) {
-    swz_fill_chunks<T, BC, KCPR, NW>(sK[stage], wave, l, [&](int r, int c) {
+  auto fill = [&](T* dk, T* dv, int kt) {
+    swz_fill_chunks<T, BC, KCPR, NW>(dk, wave, l, [&](int r, int c) {
       const size_t row = (size_t)(b * S + min(kt + r, S - 1));
       return c < NCPR ? kv + (row * H + h) * DKVH + c * 8 : kpe + row * DR + (c - NCPR) * 8;
     });
-    swz_fill<T, BC, VCPR, NW>(sV[stage], wave, l, [&](int r) {
+    swz_fill<T, BC, VCPR, NW>(dv, wave, l, [&](int r) {
       return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH + DN;
     });
   };
 
   const int ntiles = (kend + BC - 1) / BC;
-  for (int t = 0; t < NS - 1 && t < ntiles; ++t) fill(t, t * BC);
-  for (int it = 0; it < ntiles; ++it) {
-    const int kt = it * BC, st = it % NS;
-    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));
-    __syncthreads();  // tile `it` has landed for all waves; stage (it - 1) % NS is free
-    if (it + NS - 1 < ntiles) fill((it + NS - 1) % NS, (it + NS - 1) * BC);
-    const T* tk = sK[st];
-    const T* tv = sV[st];
+  fill(sK0, sV0, 0);
+  auto step = [&](auto stage, int it) {
+    constexpr int ST = decltype(stage)::value;
+    const int kt = it * BC;
+    wait_vmem();      // this wave's loads of tile `it` (and, the first time, of dO) have landed
+    __syncthreads();  // ... and everyone's; the other stage is free
+    if (it + 1 < ntiles) {
+      if constexpr (ST == 0) fill(sK1, sV1, kt + BC);
+      else fill(sK0, sV0, kt + BC);
+    }
+    const T* tk = ST == 0 ? sK0 : sK1;
+    const T* tv = ST == 0 ? sV0 : sV1;
 
     f32x16 sa[BC / 32], dp[BC / 32];
 #pragma unroll
@@ -274,6 +281,10 @@ __global__ __launch_bounds__(64 * WPH, 2) void dq_ring_kernel(BwdParams P) {
 #pragma unroll
       for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], swz_tr_frag<KCPR>(tk, ra, ra + 8, db * 32), zf);
     }
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
 
   if (my_q >= S) return;
@@ -297,7 +308,7 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   constexpr int BR = 32 * Tl::WPH_Q;
   P.n_blocks = (P.S + BR - 1) / BR;
   if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128)
-    dq_ring_kernel<DN, DR, DV, 32, Tl::WPH_Q, 2><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
+    dq_ring_kernel<DN, DR, DV, 32, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
   else
     dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
   return hipGetLastError();

@@ -17,6 +17,8 @@
 // in-lane reductions plus one exchange between lane halves, and the rescale of
 // O^T (also lane-per-query) needs no shuffles at all. Softmax runs in base 2
 // with log2(e) folded into the scale; lse is returned in natural log.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -266,16 +268,18 @@ void attn_fwd_kernel(FwdParams P) {
 // (p = 0, m and O unchanged). Softmax details: the running max is taken on the raw
 // scores (scale > 0), p = exp2(s * scale_log2 - m) is one FMA and one v_exp_f32,
 // and O^T is rescaled only when some lane's running max moved.
-template <int DN, int DR, int DV, int BC, int WPH, int NS>
+template <int DN, int DR, int DV, int BC, int WPH>
 __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, BR = 32 * WPH;
   constexpr int KCPR = DN / 8, PCPR = DR / 8, VCPR = DV / 8;
   static_assert(KCPR == 16 && PCPR == 8 && VCPR == 16, "swizzles are defined for 128/64/128-wide rows");
-  __shared__ __attribute__((aligned(16))) T sK[NS][BC * DN];
-  __shared__ __attribute__((aligned(16))) T sP[NS][BC * DR];
-  __shared__ __attribute__((aligned(16))) T sV[NS][BC * DV];
-  constexpr int F = (BC * (KCPR + VCPR + PCPR) / 64) / NW;  // load instructions per wave per tile
+  // two ring stages as distinct LDS objects: the compiler then sees that the direct
+  // loads into one stage cannot alias the reads of the other and does not wait for
+  // them (the explicit wait + barrier at the top of each tile orders the stages)
+  __shared__ __attribute__((aligned(16))) T sK0[BC * DN], sK1[BC * DN];
+  __shared__ __attribute__((aligned(16))) T sP0[BC * DR], sP1[BC * DR];
+  __shared__ __attribute__((aligned(16))) T sV0[BC * DV], sV1[BC * DV];
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -308,29 +312,33 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   for (int i = 0; i < DV / 32; ++i) oacc[i] = f32x16{};
   float m = -INFINITY, lsum = 0.f;
 
-  auto fill = [&](int stage, int kt) {
+  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
     // key rows past S are clamped to S-1 (valid memory) and masked below
-    swz_fill<T, BC, KCPR, NW>(sK[stage], wave, l, [&](int r) {
+    swz_fill<T, BC, KCPR, NW>(dk, wave, l, [&](int r) {
       return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH;
     });
-    swz_fill<T, BC, VCPR, NW>(sV[stage], wave, l, [&](int r) {
+    swz_fill<T, BC, VCPR, NW>(dv, wave, l, [&](int r) {
       return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH + DN;
     });
-    swz_fill<T, BC, PCPR, NW>(sP[stage], wave, l, [&](int r) {
+    swz_fill<T, BC, PCPR, NW>(dp, wave, l, [&](int r) {
       return kpe + (size_t)(b * S + min(kt + r, S - 1)) * DR;
     });
   };
 
   const int ntiles = (kend + BC - 1) / BC;
-  for (int t = 0; t < NS - 1 && t < ntiles; ++t) fill(t, t * BC);
-  for (int it = 0; it < ntiles; ++it) {
-    const int kt = it * BC, st = it % NS;
-    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));
-    __syncthreads();  // tile `it` has landed for all waves; stage (it - 1) % NS is free
-    if (it + NS - 1 < ntiles) fill((it + NS - 1) % NS, (it + NS - 1) * BC);
-    const T* tk = sK[st];
-    const T* tp = sP[st];
-    const T* tv = sV[st];
+  fill(sK0, sP0, sV0, 0);
+  auto step = [&](auto stage, int it) {
+    constexpr int ST = decltype(stage)::value;
+    const int kt = it * BC;
+    wait_vmem();      // this wave's loads of tile `it` have landed
+    __syncthreads();  // ... and everyone's; the other stage is free
+    if (it + 1 < ntiles) {
+      if constexpr (ST == 0) fill(sK1, sP1, sV1, kt + BC);
+      else fill(sK0, sP0, sV0, kt + BC);
+    }
+    const T* tk = ST == 0 ? sK0 : sK1;
+    const T* tp = ST == 0 ? sP0 : sP1;
+    const T* tv = ST == 0 ? sV0 : sV1;
 
     f32x16 sacc[BC / 32];
 #pragma unroll
@@ -387,6 +395,10 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
         const int ra = kk * 16 + 4 * g;
         mma(oacc[db], swz_tr_frag<VCPR>(tv, ra, ra + 8, db * 32), pf[kk]);
       }
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
 
   if (my_q >= S) return;
@@ -626,7 +638,7 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * P.n_hgroups, a.B, 1);
   if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128 && Tl::G == 1) {
-    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, Tl::WPH, 2><<<grid, 64 * Tl::WPH, 0, st>>>(P);
+    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, Tl::WPH><<<grid, 64 * Tl::WPH, 0, st>>>(P);
   } else {
     using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
     attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);

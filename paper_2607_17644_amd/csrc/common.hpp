@@ -144,24 +144,30 @@ __device__ __forceinline__ void ring_wait(int ahead) {
 // A "swizzled tile" is R rows x CPR 16-byte chunks stored without padding; logical
 // chunk c of row r lives at physical chunk c ^ swz<CPR>(r) of that row. Without
 // padding, a wave instruction of direct global->LDS loads fills 64 consecutive
-// chunks, and the XOR keeps both access patterns of the kernels free of LDS bank
-// conflicts (64 banks x 4 bytes; 16 lanes are serviced per cycle):
-//   * 16-byte row fragments: 16 lanes read one logical chunk of 16 consecutive rows;
-//   * ds_read_b64_tr_b16: a 16-lane group reads 2 adjacent chunks (c even) of 4
-//     consecutive rows starting at a multiple of 4.
-// CPR = 16 (256-byte rows): swz is a bit permutation of r & 15 whose bits 1-2 come
-//   from r & 3, so 16 consecutive rows hit 16 distinct chunks and 4 consecutive
-//   rows never share a chunk pair.
-// CPR = 24 (384-byte rows, odd rows on the other half of the banks): 3-bit swz,
-//   distinct over the 8 rows of each parity among 16 consecutive rows, and rows
-//   r, r+2 (r % 4 == 0) differ in bit 2.
-// CPR = 8 (128-byte rows, rows of equal parity share bank halves): the CPR = 24 rule.
+// chunks, and the XOR keeps the kernels' LDS reads free of bank conflicts (64 banks
+// x 4 bytes; measured on gfx950: 16-byte reads are serviced 16 lanes per cycle,
+// ds_read_b64_tr_b16 32 lanes per cycle). The access patterns, rows aligned as shown:
+//   (a) 16-byte row fragments: one logical chunk of 16 consecutive rows (aligned 16);
+//   (b) 32x32 transposing reads: 4 consecutive chunks c..c+3 (c % 4 == 0) of 4 rows
+//       (aligned 4);
+//   (c) 16x16 transposing reads: 2 chunks c, c+1 (c even) of 8 rows (aligned 8).
+// CPR = 16 (256-byte rows, every row starts at bank 0): with r = (r3 r2 r1 r0),
+//   swz = (r1 r0 r2 r3): a bijection on 16 rows (a); bits 3-2 = (r1 r0) differ over
+//   4 aligned rows (b); bits 3-1 = (r1 r0 r2) differ over 8 aligned rows (c).
+// CPR = 24 and CPR = 8 (384- and 128-byte rows: odd rows start half-way round the
+//   banks, so only rows of equal parity can collide): swz = (r1 r2 r3), a bijection
+//   on the 8 rows of either parity among 16 (a); bit 2 = r1 differs between rows r
+//   and r + 2 (b); bits 2-1 = (r1 r2) differ over the 4 rows of a parity among 8 (c).
 template <int CPR> __device__ __forceinline__ int swz(int r);
 template <> __device__ __forceinline__ int swz<16>(int r) {
-  return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+  return ((r & 2) << 2) | ((r & 1) << 2) | ((r & 4) >> 1) | ((r >> 3) & 1);
 }
-template <> __device__ __forceinline__ int swz<24>(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
-template <> __device__ __forceinline__ int swz<8>(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+template <> __device__ __forceinline__ int swz<24>(int r) {
+  return ((r & 2) << 1) | ((r & 4) >> 1) | ((r >> 3) & 1);
+}
+template <> __device__ __forceinline__ int swz<8>(int r) {
+  return ((r & 2) << 1) | ((r & 4) >> 1) | ((r >> 3) & 1);
+}
 
 // Element offset of (row, element col) in a swizzled tile of CPR chunks per row.
 template <typename T, int CPR>
@@ -187,6 +193,29 @@ __device__ __forceinline__ bf16x8 swz_tr_frag(const bf16* tile, int ra, int rb, 
   const int r0 = ra + (s >> 2), r1 = rb + (s >> 2);
   const bf16* pa = tile + swz_off<bf16, CPR>(r0, col);
   const bf16* pb = tile + swz_off<bf16, CPR>(r1, col);
+  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
+  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// 16x16x32 bf16 MFMA (one 16x16 output block, contraction over 32): lane l serves
+// row/column (l % 16) of its operand and contraction indices 8 * (l / 16) .. +7;
+// its 4 accumulators hold output column (l % 16) at rows 4 * (l / 16) + e.
+__device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+
+// Transposing fragment for the 16x16x32 shape from a swizzled bf16 tile X: every
+// 16-lane group reads the same 16 columns c0 .. c0+15; lane l returns X[ra + e][c0 +
+// l%16] (e = 0..3) and X[rb + e][c0 + l%16] (e = 0..3), ra and rb per lane (they
+// normally depend on the group l / 16), both multiples of 4.
+template <int CPR>
+__device__ __forceinline__ bf16x8 swz_tr_frag16(const bf16* tile, int ra, int rb, int c0) {
+  const int s = threadIdx.x & 15;
+  const int col = c0 + 4 * (s & 3);
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const bf16* pa = tile + swz_off<bf16, CPR>(ra + (s >> 2), col);
+  const bf16* pb = tile + swz_off<bf16, CPR>(rb + (s >> 2), col);
   bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
   bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
