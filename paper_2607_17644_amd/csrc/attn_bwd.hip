@@ -273,165 +273,13 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 }
 
 
-// Key-stationary backward, bf16 with 192/128-wide heads: the query tiles (Q, dO and
-// the per-row lse2 / delta) stream through a two-stage LDS ring filled by direct
-// global->LDS loads into swizzled, unpadded tiles, so no registers are spent on
-// staging and one barrier per tile suffices. Math as in dkdv_kernel.
-template <int DN, int DR, int DV, int WPH, int NS>
-__global__ __launch_bounds__(64 * WPH) void dkdv_ring_kernel(BwdParams P) {
-  using T = bf16;
-  constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 32 * WPH;
-  constexpr int QCPR = DQK / 8, OCPR = DV / 8;  // 16-byte chunks per row
-  static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
-  __shared__ __attribute__((aligned(16))) T sQ[NS][BQ * DQK];
-  __shared__ __attribute__((aligned(16))) T sO[NS][BQ * DV];
-  __shared__ __attribute__((aligned(16))) float sLD[NS][2 * BQ];  // lse2 then delta
-  constexpr int F = (BQ * (QCPR + OCPR) / 64) / NW;  // load instructions per wave per tile (at least)
-
-  const T* __restrict__ q = (const T*)P.q;
-  const T* __restrict__ kpe = (const T*)P.k_pe;
-  const T* __restrict__ kv = (const T*)P.kv;
-  const T* __restrict__ dout = (const T*)P.dout;
-  const int S = P.S, H = P.H;
-
-  const int total = P.n_blocks * H * gridDim.y;
-  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
-  const int kb = lin % P.n_blocks;
-  const int bh = lin / P.n_blocks;
-  const int b = bh / H, h = bh % H;
-
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
-  const int k0 = kb * BK + wave * 32;
-  const int my_k = k0 + n;
-
-  frag_t<T> kf[DQK / 16], vf[DV / 16];
-  {
-    const bool ok = my_k < S;
-    const size_t row = (size_t)(b * S + (ok ? my_k : 0));
-    const T* kvr = kv + (row * H + h) * DKVH;
-#pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) {
-      const T* src = ks < DN / 16 ? kvr + ks * 16 + 8 * g : kpe + row * DR + (ks - DN / 16) * 16 + 8 * g;
-      kf[ks] = *reinterpret_cast<const frag_t<T>*>(src);
-      if (!ok) kf[ks] = frag_t<T>{};
-    }
-#pragma unroll
-    for (int ks = 0; ks < DV / 16; ++ks) {
-      vf[ks] = *reinterpret_cast<const frag_t<T>*>(kvr + DN + ks * 16 + 8 * g);
-      if (!ok) vf[ks] = frag_t<T>{};
-    }
-  }
-
-  f32x16 dk[DQK / 32], dv[DV / 32];
-#pragma unroll
-  for (int i = 0; i < DQK / 32; ++i) dk[i] = f32x16{};
-#pragma unroll
-  for (int i = 0; i < DV / 32; ++i) dv[i] = f32x16{};
-
-  const size_t hrow = (size_t)(b * H + h) * P.S_pad;
-  auto fill = [&](int stage, int qt) {
-    // rows past S are clamped to S-1 (valid memory); their P is masked to zero
-    swz_fill<T, BQ, QCPR, NW>(sQ[stage], wave, l, [&](int r) {
-      const int qi = min(qt + r, S - 1);
-      return q + ((size_t)(b * S + qi) * H + h) * DQK;
-    });
-    swz_fill<T, BQ, OCPR, NW>(sO[stage], wave, l, [&](int r) {
-      const int qi = min(qt + r, S - 1);
-      return dout + ((size_t)(b * S + qi) * H + h) * DV;
-    });
-    if (wave == NW - 1 && l < 2 * BQ / 4) {  // 8 chunks of lse2, then 8 of delta (padded rows)
-      const float* src = l < BQ / 4 ? P.lse2 + hrow + qt + 4 * l : P.delta + hrow + qt + 4 * (l - BQ / 4);
-      g2lds16(src, &sLD[stage][0]);
-    }
-  };
-
-  const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
-  const int ntiles = (S - qt_begin + BQ - 1) / BQ;
-  for (int t = 0; t < NS - 1 && t < ntiles; ++t) fill(t, qt_begin + t * BQ);
-  for (int it = 0; it < ntiles; ++it) {
-    const int qt = qt_begin + it * BQ, st = it % NS;
-    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));
-    __syncthreads();  // tile `it` has landed for all waves; stage (it - 1) % NS is free
-    if (it + NS - 1 < ntiles) fill((it + NS - 1) % NS, qt_begin + (it + NS - 1) * BQ);
-
-    // waves whose keys all lie after this tile's queries run it fully masked (P = 0):
-    // keeping the loop body free of per-wave branches keeps the accumulators in place
-    const bool need_mask = (P.causal && qt < k0 + 31) || (qt + BQ > S);
-    const T* tq = sQ[st];
-    const T* to = sO[st];
-
-    f32x16 sa{}, dp{};
-#pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) mma(sa, swz_frag<T, QCPR>(tq, n, 2 * ks + g), kf[ks]);
-#pragma unroll
-    for (int ks = 0; ks < DV / 16; ++ks) mma(dp, swz_frag<T, OCPR>(to, n, 2 * ks + g), vf[ks]);
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int qrow = rr * 8 + g * 4;
-      const f32x4 lq = *reinterpret_cast<const f32x4*>(&sLD[st][qrow]);
-      const f32x4 dq = *reinterpret_cast<const f32x4*>(&sLD[st][BQ + qrow]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = rr * 4 + e;
-        float p = fast_exp2(sa[r] * P.scale_log2 - lq[e]);
-        if (need_mask) {
-          const int qi = qt + qrow + e;
-          if (qi >= S || (P.causal && my_k > qi)) p = 0.f;
-        }
-        sa[r] = p;
-        dp[r] = p * (dp[r] - dq[e]);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < BQ / 16; ++kk) {
-      const frag_t<T> pf = acc_to_frag<T>(sa, kk);
-      const frag_t<T> zf = acc_to_frag<T>(dp, kk);
-      const int ra = kk * 16 + 4 * g;
-#pragma unroll
-      for (int db = 0; db < DV / 32; ++db) mma(dv[db], swz_tr_frag<OCPR>(to, ra, ra + 8, db * 32), pf);
-#pragma unroll
-      for (int db = 0; db < DQK / 32; ++db) mma(dk[db], swz_tr_frag<QCPR>(tq, ra, ra + 8, db * 32), zf);
-    }
-  }
-
-  if (my_k >= S) return;
-  const size_t row = (size_t)(b * S + my_k) * H + h;
-  T* dkvr = (T*)P.dkv + row * DKVH;
-  T* dkvl = (T*)P.dkv_lo + row * DKVH;
-  float* dper = P.dkpe_h + row * DR;
-  auto put4 = [&](int col, float a0, float a1, float a2, float a3) {
-    bf16x4 hi = {to_elem<T>(a0), to_elem<T>(a1), to_elem<T>(a2), to_elem<T>(a3)};
-    bf16x4 lo = {to_elem<T>(a0 - to_f32(hi[0])), to_elem<T>(a1 - to_f32(hi[1])), to_elem<T>(a2 - to_f32(hi[2])),
-                 to_elem<T>(a3 - to_f32(hi[3]))};
-    *reinterpret_cast<bf16x4*>(dkvr + col) = hi;
-    *reinterpret_cast<bf16x4*>(dkvl + col) = lo;
-  };
-#pragma unroll
-  for (int db = 0; db < DQK / 32; ++db)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int d = db * 32 + rr * 8 + g * 4;
-      const float a0 = dk[db][4 * rr] * P.scale, a1 = dk[db][4 * rr + 1] * P.scale;
-      const float a2 = dk[db][4 * rr + 2] * P.scale, a3 = dk[db][4 * rr + 3] * P.scale;
-      if (d < DN) {
-        put4(d, a0, a1, a2, a3);
-      } else {
-        f32x4 v = {a0, a1, a2, a3};
-        *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
-      }
-    }
-#pragma unroll
-  for (int db = 0; db < DV / 32; ++db)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
-      put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
-}
-
 // Key-stationary backward with 16 keys per wave on the 16x16x32 MFMA: the per-wave
 // state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
 // the 32-key layout, so two waves share each SIMD and hide each other's latencies.
 // A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
-// stream through an NS-stage LDS ring (direct global->LDS loads, swizzled tiles).
+// stream through a two-stage LDS ring of direct global->LDS loads into padded tiles
+// (pitch = row + 2 chunks: conflict-free for both 16x16 read patterns, and every read
+// is a per-lane base address plus a constant, which keeps the kernel at ~200 VGPRs).
 //   S = Q K^T, dP = dO V^T: A = Q / dO rows (16-byte row fragments), B = the lane's
 //       key / value row; accumulator: lane <-> key, 4 queries per 16-query block.
 //   dV^T += dO^T P, dK^T += Q^T dZ: the contraction over the tile's 32 queries takes
@@ -442,11 +290,12 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 16 * WPH;
   constexpr int QCPR = DQK / 8, OCPR = DV / 8;
-  static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
+  static_assert(QCPR % 4 == 0 && OCPR % 4 == 0, "padded pitches assume rows of whole 64-byte groups");
   // two ring stages as distinct LDS objects (so the compiler does not make the reads
   // of one stage wait for the direct loads into the other)
-  __shared__ __attribute__((aligned(16))) T sQ0[BQ * DQK], sQ1[BQ * DQK];
-  __shared__ __attribute__((aligned(16))) T sO0[BQ * DV], sO1[BQ * DV];
+  constexpr int QP = QCPR + 2, OP = OCPR + 2;  // pitches in chunks, P % 4 == 2
+  __shared__ __attribute__((aligned(16))) T sQ0[BQ * QP * 8], sQ1[BQ * QP * 8];
+  __shared__ __attribute__((aligned(16))) T sO0[BQ * OP * 8], sO1[BQ * OP * 8];
   __shared__ __attribute__((aligned(16))) float sLD0[2 * BQ], sLD1[2 * BQ];  // lse2 then delta
 
   const T* __restrict__ q = (const T*)P.q;
@@ -492,10 +341,10 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 
   const size_t hrow = (size_t)(b * H + h) * P.S_pad;
   auto fill = [&](T* dq_, T* do_, float* dld, int qt) {
-    swz_fill<T, BQ, QCPR, NW>(dq_, wave, l, [&](int r) {
+    pad_fill<T, BQ, QCPR, QP, NW>(dq_, wave, l, [&](int r) {
       return q + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DQK;
     });
-    swz_fill<T, BQ, OCPR, NW>(do_, wave, l, [&](int r) {
+    pad_fill<T, BQ, OCPR, OP, NW>(do_, wave, l, [&](int r) {
       return dout + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DV;
     });
     if (wave == NW - 1 && l < 2 * BQ / 4) {
@@ -527,9 +376,9 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
       sa[qb] = f32x4{};
       dp[qb] = f32x4{};
 #pragma unroll
-      for (int ks = 0; ks < DQK / 32; ++ks) mma16(sa[qb], swz_frag<T, QCPR>(tq, qb * 16 + j, 4 * ks + G), kf[ks]);
+      for (int ks = 0; ks < DQK / 32; ++ks) mma16(sa[qb], pad_frag<QP>(tq, qb * 16 + j, 4 * ks + G), kf[ks]);
 #pragma unroll
-      for (int ks = 0; ks < DV / 32; ++ks) mma16(dp[qb], swz_frag<T, OCPR>(to, qb * 16 + j, 4 * ks + G), vf[ks]);
+      for (int ks = 0; ks < DV / 32; ++ks) mma16(dp[qb], pad_frag<OP>(to, qb * 16 + j, 4 * ks + G), vf[ks]);
     }
     bf16x8 pf, zf;
 #pragma unroll
@@ -550,9 +399,9 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     }
     const int ra = 4 * G, rb = 16 + 4 * G;
 #pragma unroll
-    for (int db = 0; db < DV / 16; ++db) mma16(dv[db], swz_tr_frag16<OCPR>(to, ra, rb, db * 16), pf);
+    for (int db = 0; db < DV / 16; ++db) mma16(dv[db], pad_tr_frag16<OP>(to, ra, rb, db * 16), pf);
 #pragma unroll
-    for (int db = 0; db < DQK / 16; ++db) mma16(dk[db], swz_tr_frag16<QCPR>(tq, ra, rb, db * 16), zf);
+    for (int db = 0; db < DQK / 16; ++db) mma16(dk[db], pad_tr_frag16<QP>(tq, ra, rb, db * 16), zf);
   };
   for (int it = 0; it < ntiles; it += 2) {
     step(std::integral_constant<int, 0>{}, it);

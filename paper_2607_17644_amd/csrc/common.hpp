@@ -140,24 +140,29 @@ __device__ __forceinline__ void ring_wait(int ahead) {
   else wait_vmem();
 }
 
-// ---------------------------------------------------------------- swizzled tiles
+// ---------------------------------------------------------------- LDS tile layouts
+// Bank model (64 banks x 4 bytes, measured on gfx950 with lane-pair probes): a read
+// costs an extra pass whenever two lanes of one pass touch one bank at different
+// addresses.
+//   ds_read_b128: four passes of 16 lanes, pass = (lane bit 5, parity of lane bits
+//     2..4), i.e. lanes {0-3, 12-15, 20-23, 24-27} and {4-11, 16-19, 28-31} for the
+//     lower half-wave and likewise for the upper one.
+//   ds_read_b64_tr_b16: two passes of 32 lanes (the half-waves).
+// Read patterns of the kernels, by MFMA shape:
+//   32x32x16 operands: (a) 16-byte row fragments, logical chunk c (even) of 32
+//     consecutive rows in one half-wave and c+1 in the other; (b) transposing reads
+//     of 4 chunks c..c+3 (c % 4 == 0) of 4 rows per 16 lanes, rows ra + {0, 8}.
+//   16x16x32 operands: (a) 16-byte row fragments, chunk c + l/16 (c % 4 == 0) of 16
+//     consecutive rows; (b) transposing reads of 2 chunks c, c+1 (c even) of 4 rows
+//     per 16 lanes, rows {4G, 16 + 4G}.
+//
 // A "swizzled tile" is R rows x CPR 16-byte chunks stored without padding; logical
 // chunk c of row r lives at physical chunk c ^ swz<CPR>(r) of that row. Without
-// padding, a wave instruction of direct global->LDS loads fills 64 consecutive
-// chunks, and the XOR keeps the kernels' LDS reads free of bank conflicts (64 banks
-// x 4 bytes; measured on gfx950: 16-byte reads are serviced 16 lanes per cycle,
-// ds_read_b64_tr_b16 32 lanes per cycle). The access patterns, rows aligned as shown:
-//   (a) 16-byte row fragments: one logical chunk of 16 consecutive rows (aligned 16);
-//   (b) 32x32 transposing reads: 4 consecutive chunks c..c+3 (c % 4 == 0) of 4 rows
-//       (aligned 4);
-//   (c) 16x16 transposing reads: 2 chunks c, c+1 (c even) of 8 rows (aligned 8).
-// CPR = 16 (256-byte rows, every row starts at bank 0): with r = (r3 r2 r1 r0),
-//   swz = (r1 r0 r2 r3): a bijection on 16 rows (a); bits 3-2 = (r1 r0) differ over
-//   4 aligned rows (b); bits 3-1 = (r1 r0 r2) differ over 8 aligned rows (c).
-// CPR = 24 and CPR = 8 (384- and 128-byte rows: odd rows start half-way round the
-//   banks, so only rows of equal parity can collide): swz = (r1 r2 r3), a bijection
-//   on the 8 rows of either parity among 16 (a); bit 2 = r1 differs between rows r
-//   and r + 2 (b); bits 2-1 = (r1 r2) differ over the 4 rows of a parity among 8 (c).
+// padding, a wave instruction of direct global->LDS loads fills 64 consecutive chunks.
+// The XOR values below make both 32x32 patterns conflict-free (checked exhaustively
+// under the model above; rows of 384 bytes start half-way round the banks on odd
+// rows, rows of 256 bytes all start at bank 0). They are used for tiles read both
+// ways (a) and (b); tiles read only one way use padded tiles (below).
 template <int CPR> __device__ __forceinline__ int swz(int r);
 template <> __device__ __forceinline__ int swz<16>(int r) {
   return ((r & 2) << 2) | ((r & 1) << 2) | ((r & 4) >> 1) | ((r >> 3) & 1);
@@ -205,22 +210,6 @@ __device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8&
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
 }
 
-// Transposing fragment for the 16x16x32 shape from a swizzled bf16 tile X: every
-// 16-lane group reads the same 16 columns c0 .. c0+15; lane l returns X[ra + e][c0 +
-// l%16] (e = 0..3) and X[rb + e][c0 + l%16] (e = 0..3), ra and rb per lane (they
-// normally depend on the group l / 16), both multiples of 4.
-template <int CPR>
-__device__ __forceinline__ bf16x8 swz_tr_frag16(const bf16* tile, int ra, int rb, int c0) {
-  const int s = threadIdx.x & 15;
-  const int col = c0 + 4 * (s & 3);
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  const bf16* pa = tile + swz_off<bf16, CPR>(ra + (s >> 2), col);
-  const bf16* pb = tile + swz_off<bf16, CPR>(rb + (s >> 2), col);
-  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
-  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
-  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
 // Direct global->LDS fill of a swizzled tile of NROWS x CPR chunks by NW waves:
 // wave instruction j covers physical chunks [64 j, 64 j + 64); lane i fetches the
 // logical chunk that belongs at physical chunk 64 j + i, i.e. c = p ^ swz(row), from
@@ -245,6 +234,60 @@ template <typename T, int NROWS, int CPR, int NW, typename RowPtr>
 __device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_ptr) {
   constexpr int E = 16 / sizeof(T);
   swz_fill_chunks<T, NROWS, CPR, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
+}
+
+// ---------------------------------------------------------------- padded tiles
+// A "padded tile" holds NROWS rows of CPR 16-byte chunks at a pitch of P chunks (P - CPR
+// chunks of padding at the end of each row). Unlike an XOR swizzle, padding keeps every
+// LDS read of a lane at its own base address plus a compile-time offset, which saves
+// registers and per-read address arithmetic. Conflict-free pitches under the bank
+// model (checked exhaustively over chunk offsets and row blocks):
+//   16x16x32 operands (both patterns): P % 4 == 2 (CPR 16 -> 18, CPR 24 -> 26);
+//   32x32 16-byte row fragments only: P odd (CPR 8 -> 9, 16 -> 17, 24 -> 25);
+//   32x32 transposing reads only: P % 8 == 4 (CPR 16 -> 20, 24 -> 28);
+// no pitch serves both 32x32 patterns; a tile read both ways keeps the XOR swizzle.
+//
+// Chunks to allocate for a padded tile: NROWS * P rounded up to whole wave
+// instructions of direct loads (64 chunks).
+__host__ __device__ constexpr int pad_chunks(int nrows, int p) { return (nrows * p + 63) / 64 * 64; }
+
+// Direct global->LDS fill by NW waves: wave instruction j covers physical chunks
+// [64 j, 64 j + 64); lane i serves physical chunk p = 64 j + i, i.e. row p / P,
+// chunk p % P. Lanes on padding, or past the last row (the allocation is rounded up
+// to pad_chunks), reload chunk 0 of row 0 / of their row; those chunks are never read.
+template <typename T, int NROWS, int CPR, int P, int NW, typename RowPtr>
+__device__ __forceinline__ void pad_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+  constexpr int E = 16 / sizeof(T);
+  constexpr int NI = pad_chunks(NROWS, P) / 64;
+#pragma unroll
+  for (int j = wave; j < NI; j += NW) {
+    const int p = j * 64 + l;
+    int row = p / P, c = p % P;
+    if (NI * 64 > NROWS * P && row >= NROWS) row = 0;
+    g2lds16(row_ptr(row) + (c < CPR ? c : 0) * E, tile + j * 64 * E);
+  }
+}
+
+// 16-byte row fragment: chunk c of `row` of a padded bf16 tile.
+template <int P>
+__device__ __forceinline__ bf16x8 pad_frag(const bf16* tile, int row, int c) {
+  return *reinterpret_cast<const bf16x8*>(tile + (row * P + c) * 8);
+}
+
+// Transposing fragment for the 16x16x32 shape from a padded bf16 tile: every 16-lane
+// group reads the same 16 columns c0 .. c0+15; lane l returns X[ra + e][c0 + l%16]
+// (e = 0..3) and X[rb + e][c0 + l%16] (e = 0..3), ra and rb per lane (they normally
+// depend on the group l / 16), both multiples of 4.
+template <int P>
+__device__ __forceinline__ bf16x8 pad_tr_frag16(const bf16* tile, int ra, int rb, int c0) {
+  const int s = threadIdx.x & 15;
+  const int col = c0 + 4 * (s & 3);
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const bf16* pa = tile + (ra + (s >> 2)) * P * 8 + col;
+  const bf16* pb = tile + (rb + (s >> 2)) * P * 8 + col;
+  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
+  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // Zero value of a 16-byte staging chunk.
