@@ -144,7 +144,11 @@ LAGA_API laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q,
  *   LAGA_BWD_PREPARE  per-row delta = sum(dout * out) (and the K/V rebuild of
  *                     the FUSED mode when kv is NULL)
  *   LAGA_BWD_DKDV     key-stationary attention backward: dK, dV of every key
- *   LAGA_BWD_DQ       query-stationary attention backward: dq
+ *                     (bf16 with 192/128-wide heads: also stores dS^T of every
+ *                     causal pair, bf16, in the workspace)
+ *   LAGA_BWD_DQ       attention backward for dq (bf16 with 192/128-wide heads:
+ *                     the product K^T dS^T over the stored dS^T; otherwise a
+ *                     query-stationary pass that recomputes the scores)
  *   LAGA_BWD_FINISH   dk_pe head sum, dc_kv and dw_kv_b up-projection GEMMs
  * Each stage reads what the previous ones left in the workspace. */
 typedef enum {
@@ -164,7 +168,10 @@ LAGA_API laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p,
                                            size_t workspace_bytes, void* stream);
 
 /* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
- * is invalid (check with the entry point itself for the error code). */
+ * is invalid (check with the entry point itself for the error code). For the
+ * backward in bf16 with 192/128-wide heads this includes the dS^T store:
+ * 2 * B * H * 512 * T * (T + 1) bytes with the causal mask (2 * B * H * 1024 * T^2
+ * without), T = ceil(S / 32) -- about 4.3 GB at S = 16384, H = 16. */
 LAGA_API size_t laga_workspace_bytes(const laga_problem_t* p, int op);
 
 /* Static, never-NULL description of a status code. */

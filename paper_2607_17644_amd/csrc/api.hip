@@ -5,6 +5,7 @@
 
 #include "laga.h"
 #include "kernels.hpp"
+#include "bwd_common.hpp"
 
 using namespace laga;
 
@@ -51,10 +52,12 @@ size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ?
 
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials | kv rebuild]
+// Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials |
+// kv rebuild | dS^T store (bf16 with 192/128-wide heads)]
 struct BwdWs {
-  size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, total;
+  size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, ds, total;
 };
+bool stores_ds(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 && is_v3(p); }
 int s_pad(int S) { return (S + kRowPad - 1) / kRowPad * kRowPad; }
 BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   BwdWs w{};
@@ -68,6 +71,8 @@ BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   const size_t ns = dw_split_count((int)tok);
   w.dw_part = off; off += ns > 1 ? round_up(sizeof(float) * ns * d.d_c * d.H * d.dkvh()) : 0;
   w.kv = off; off += p->kv_mode == LAGA_KV_FUSED ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
+  w.ds = off;
+  off += stores_ds(p) ? round_up(sizeof(uint16_t) * (size_t)d.B * d.H * bwd::ds_head_elems((d.S + 31) / 32, p->causal)) : 0;
   w.total = off;
   return w;
 }
@@ -194,6 +199,7 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
   a.lse2 = (float*)(wsb + ws.lse2); a.S_pad = s_pad(d.S);
   a.dkv_lo = bf ? wsb + ws.dkv_lo : nullptr;
   a.dk_pe = dk_pe;
+  a.ds = stores_ds(p) ? wsb + ws.ds : nullptr;
   a.B = d.B; a.S = d.S; a.H = d.H; a.scale = p->softmax_scale; a.causal = p->causal;
   hipError_t e;
   const int kstage = stage == LAGA_BWD_PREPARE ? 0 : stage == LAGA_BWD_DKDV ? 1 : stage == LAGA_BWD_DQ ? 2 : 3;

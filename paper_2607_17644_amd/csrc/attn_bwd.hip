@@ -353,14 +353,30 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     }
   };
 
+  // dS^T of a tile for the dQ pass: key my_k's row of 32 queries; the lane holds
+  // queries {4G..4G+3} and {16+4G..16+4G+3}. Only the keys the tile sees are stored.
+  // The store of tile i is issued after the barrier of tile i + 1, ahead of that
+  // tile's loads, so the wait for those loads also covers it and its latency hides
+  // behind a whole tile (vector-memory stores and loads share one counter).
+  bf16x8 zs{};
+  int ts = -1;
+  auto store_ds = [&]() {
+    if (ts >= 0 && my_k < ds_tile_keys(P.ds_T, P.causal, ts)) {
+      T* dsr = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, ts) + (size_t)my_k * BQ;
+      *reinterpret_cast<bf16x4*>(dsr + 4 * G) = __builtin_shufflevector(zs, zs, 0, 1, 2, 3);
+      *reinterpret_cast<bf16x4*>(dsr + 16 + 4 * G) = __builtin_shufflevector(zs, zs, 4, 5, 6, 7);
+    }
+  };
+
   const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
   const int ntiles = (S - qt_begin + BQ - 1) / BQ;
   fill(sQ0, sO0, sLD0, qt_begin);
   auto step = [&](auto stage, int it) {
     constexpr int ST = decltype(stage)::value;
     const int qt = qt_begin + it * BQ;
-    wait_vmem();      // this wave's loads of tile `it` have landed
+    wait_vmem();      // this wave's loads of tile `it` (and stores of tile it - 2) are done
     __syncthreads();  // ... and everyone's; the other stage is free
+    store_ds();       // tile it - 1
     if (it + 1 < ntiles) {
       if constexpr (ST == 0) fill(sQ1, sO1, sLD1, qt + BQ);
       else fill(sQ0, sO0, sLD0, qt + BQ);
@@ -368,7 +384,9 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     const T* tq = ST == 0 ? sQ0 : sQ1;
     const T* to = ST == 0 ? sO0 : sO1;
     const float* tld = ST == 0 ? sLD0 : sLD1;
-    const bool need_mask = (P.causal && qt < k0 + 15) || (qt + BQ > S);
+    // masked: queries past S, keys past S (their dS is stored as zeros) and, causally,
+    // keys after the query
+    const bool need_mask = (P.causal && qt < k0 + 15) || (qt + BQ > S) || (k0 + 16 > S);
 
     f32x4 sa[2], dp[2];
 #pragma unroll
@@ -391,12 +409,14 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
         float p = fast_exp2(__builtin_fmaf(sa[qb][e], P.scale_log2, -lq[e]));
         if (need_mask) {
           const int qi = qt + qrow + e;
-          if (qi >= S || (P.causal && my_k > qi)) p = 0.f;
+          if (qi >= S || my_k >= S || (P.causal && my_k > qi)) p = 0.f;
         }
         pf[qb * 4 + e] = to_elem<T>(p);
         zf[qb * 4 + e] = to_elem<T>(p * (dp[qb][e] - dq[e]));
       }
     }
+    zs = zf;
+    ts = qt / BQ;
     const int ra = 4 * G, rb = 16 + 4 * G;
 #pragma unroll
     for (int db = 0; db < DV / 16; ++db) mma16(dv[db], pad_tr_frag16<OP>(to, ra, rb, db * 16), pf);
@@ -407,6 +427,7 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
+  store_ds();  // the last tile
 
   if (my_k >= S) return;
   const size_t row = (size_t)(b * S + my_k) * H + h;
@@ -461,6 +482,7 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
   P.lse2 = a.lse2; P.S_pad = a.S_pad;
   P.dq = a.dq; P.dkv = a.dkv; P.dkv_lo = a.dkv_lo; P.dkpe_h = a.dkpe_h;
   P.S = a.S; P.H = a.H; P.scale = a.scale; P.scale_log2 = a.scale * 1.4426950408889634f; P.causal = a.causal;
+  P.ds = a.ds; P.ds_T = (a.S + 31) / 32;
   if (stage == 0) {
     const int BS = a.B * a.S;
     delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.lse, a.delta, a.lse2,

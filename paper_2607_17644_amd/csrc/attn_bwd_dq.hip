@@ -1,6 +1,6 @@
-// Query-stationary dQ pass of the attention backward (gfx950); see attn_bwd.hip for
-// the whole backward. Built with MFMA results kept in VGPRs (the dZ arithmetic on
-// the dP accumulators then needs no AGPR<->VGPR copies).
+// dQ pass of the attention backward (gfx950); see attn_bwd.hip for the whole backward.
+// Built with MFMA results kept in VGPRs (the dZ arithmetic on the dP accumulators of
+// the recomputing kernel then needs no AGPR<->VGPR copies).
 #include <type_traits>
 
 #include "common.hpp"
@@ -169,125 +169,100 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
 }
 
 
-// Query-stationary dQ, bf16 with 192/128-wide heads: key tiles (K = [K_nope || k_pe]
-// as one 192-wide swizzled tile, V as a 128-wide one) stream through a two-stage
-// LDS ring of direct global->LDS loads; one barrier per tile; no per-wave branch
-// around the MFMAs (tiles entirely after a wave's queries run fully masked).
-template <int DN, int DR, int DV, int BC, int WPH>
-__global__ __launch_bounds__(64 * WPH, 2) void dq_ring_kernel(BwdParams P) {
+// dQ from the stored dS^T (bf16, 192/128-wide heads): the key-stationary pass leaves
+// dS^T = P * (dP - delta) of every causal (query tile, key) pair in the workspace, so
+// this pass is a streaming product dQ^T (192 x 32 per wave) += K^T dS^T over the
+// tile's keys, with no recomputation of S or dP. A workgroup of WPH waves owns WPH
+// consecutive 32-query tiles of one head; key blocks of 32 stream through an NS-stage
+// LDS ring of direct global->LDS loads: the K = [K_nope || k_pe] rows of the block
+// (shared, padded pitch 28 chunks) and each wave's own 32 x 32 dS^T block (64-byte
+// rows). Both MFMA operands come from transposing reads:
+//   A = K^T (lane: head dim, 8 keys), B = dS^T (lane: query, the same 8 keys).
+// Every wave issues the same number of loads per stage (the K fill is rounded up to
+// whole rounds of the workgroup, and key blocks past a wave's queries load a dummy
+// block that is not read), so the ring waits can count loads exactly.
+template <int DN, int DR, int DV, int WPH, int NS>
+__global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
   using T = bf16;
-  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, BR = 32 * WPH;
-  constexpr int KCPR = DQK / 8, VCPR = DV / 8, NCPR = DN / 8;
-  static_assert(KCPR == 24 && VCPR == 16, "swizzles are defined for 192/128-wide rows");
-  // two ring stages as distinct LDS objects (so the compiler does not make the reads
-  // of one stage wait for the direct loads into the other)
-  __shared__ __attribute__((aligned(16))) T sK0[BC * DQK], sK1[BC * DQK];
-  __shared__ __attribute__((aligned(16))) T sV0[BC * DV], sV1[BC * DV];
-  // the workgroup's dO rows stay in LDS (B operand of dP^T = V dO^T), which keeps
-  // the per-lane state small enough for two waves per SIMD
-  __shared__ __attribute__((aligned(16))) T sDO[BR * DV];
+  constexpr int DQK = DN + DR, DKVH = DN + DV, KB = 32, NW = WPH;
+  constexpr int KCPR = DQK / 8, NCPR = DN / 8, KP = KCPR + 4;  // pitch % 8 == 4
+  static_assert(KCPR % 4 == 0 && DQK % 32 == 0 && NS == 4, "192-wide K rows, four stages");
+  constexpr int KCH = (KB * KP + 64 * NW - 1) / (64 * NW) * (64 * NW);  // K chunks, whole rounds
+  constexpr int F = KCH / 64 / NW + 2;                                 // loads per wave per stage
+  __shared__ __attribute__((aligned(16))) T sK0[KCH * 8], sK1[KCH * 8], sK2[KCH * 8], sK3[KCH * 8];
+  __shared__ __attribute__((aligned(16))) T sD0[NW * KB * 32], sD1[NW * KB * 32], sD2[NW * KB * 32],
+      sD3[NW * KB * 32];
 
-  const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
   const T* __restrict__ kv = (const T*)P.kv;
-  const T* __restrict__ dout = (const T*)P.dout;
-  const int S = P.S, H = P.H;
+  const T* __restrict__ ds = (const T*)P.ds;
+  const int S = P.S, H = P.H, TT = P.ds_T;
 
   const int total = P.n_blocks * H * gridDim.y;
   const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
-  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;
+  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;  // heavy first
   const int bh = lin / P.n_blocks;
   const int b = bh / H, h = bh % H;
 
   const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
-  const int q0 = qblk * BR + wave * 32;
-  const int my_q = q0 + n;
-  const int kend = P.causal ? min(S, (qblk + 1) * BR) : S;
-
-  frag_t<T> qf[DQK / 16];
-  float lse2, dlt;
-  {
-    const bool ok = my_q < S;
-    const size_t base = (size_t)(b * S + (ok ? my_q : 0)) * H + h;
-#pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) {
-      qf[ks] = *reinterpret_cast<const frag_t<T>*>(q + base * DQK + ks * 16 + 8 * g);
-      if (!ok) qf[ks] = frag_t<T>{};
-    }
-    // dO rows of the workgroup's queries (rows past S clamped; their dq is not stored)
-    swz_fill<T, BR, VCPR, NW>(sDO, wave, l, [&](int r) {
-      return dout + ((size_t)(b * S + min(qblk * BR + r, S - 1)) * H + h) * DV;
-    });
-    const size_t hr = (size_t)(b * H + h) * P.S_pad + (ok ? my_q : 0);
-    lse2 = P.lse2[hr];
-    dlt = P.delta[hr];
-  }
+  const int t = qblk * NW + wave;  // this wave's query tile
+  const bool wave_ok = t < TT;
+  const int nk = wave_ok ? ds_tile_keys(TT, P.causal, t) : 0;  // keys stored for the tile
+  const T* dtile = ds + (wave_ok ? ds_tile_offset(TT, P.causal, bh, t) : 0);
+  const int kend = P.causal ? min(S, (qblk + 1) * NW * 32) : S;
+  const int ntiles = (kend + KB - 1) / KB;
 
   f32x16 dqa[DQK / 32];
 #pragma unroll
   for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
 
-  auto fill = [&](T* dk, T* dv, int kt) {
-    swz_fill_chunks<T, BC, KCPR, NW>(dk, wave, l, [&](int r, int c) {
+  auto fill = [&](T* dk, T* dd, int kt) {
+    pad_fill_chunks<T, KB, KCPR, KP, NW, KCH>(dk, wave, l, [&](int r, int c) {
       const size_t row = (size_t)(b * S + min(kt + r, S - 1));
       return c < NCPR ? kv + (row * H + h) * DKVH + c * 8 : kpe + row * DR + (c - NCPR) * 8;
     });
-    swz_fill<T, BC, VCPR, NW>(dv, wave, l, [&](int r) {
-      return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH + DN;
-    });
+    const T* src = kt < nk ? dtile + (size_t)kt * 32 : dtile;  // dummy block when not stored
+    g2lds16(src + l * 8, dd + wave * KB * 32);
+    g2lds16(src + 512 + l * 8, dd + wave * KB * 32 + 512);
   };
 
-  const int ntiles = (kend + BC - 1) / BC;
-  fill(sK0, sV0, 0);
+  for (int i = 0; i < NS - 1 && i < ntiles; ++i) {
+    if (i == 0) fill(sK0, sD0, 0);
+    else if (i == 1) fill(sK1, sD1, KB);
+    else fill(sK2, sD2, 2 * KB);
+  }
   auto step = [&](auto stage, int it) {
     constexpr int ST = decltype(stage)::value;
-    const int kt = it * BC;
-    wait_vmem();      // this wave's loads of tile `it` (and, the first time, of dO) have landed
-    __syncthreads();  // ... and everyone's; the other stage is free
-    if (it + 1 < ntiles) {
-      if constexpr (ST == 0) fill(sK1, sV1, kt + BC);
-      else fill(sK0, sV0, kt + BC);
+    const int kt = it * KB;
+    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));  // this wave's loads of block `it` have landed
+    __syncthreads();  // ... and everyone's; the stage filled next (read last at it - 1) is free
+    if (it + NS - 1 < ntiles) {
+      constexpr int NX = (ST + NS - 1) % NS;
+      T* nk_ = NX == 0 ? sK0 : NX == 1 ? sK1 : NX == 2 ? sK2 : sK3;
+      T* nd_ = NX == 0 ? sD0 : NX == 1 ? sD1 : NX == 2 ? sD2 : sD3;
+      fill(nk_, nd_, kt + (NS - 1) * KB);
     }
-    const T* tk = ST == 0 ? sK0 : sK1;
-    const T* tv = ST == 0 ? sV0 : sV1;
-
-    f32x16 sa[BC / 32], dp[BC / 32];
+    if (kt < nk) {  // wave-uniform: key blocks past the tile's queries hold no dS
+      const T* tk = ST == 0 ? sK0 : ST == 1 ? sK1 : ST == 2 ? sK2 : sK3;
+      const T* td = (ST == 0 ? sD0 : ST == 1 ? sD1 : ST == 2 ? sD2 : sD3) + wave * KB * 32;
 #pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb) {
-      sa[kb] = f32x16{};
-      dp[kb] = f32x16{};
+      for (int kk = 0; kk < KB / 16; ++kk) {
+        const int ra = kk * 16 + 4 * g;
+        const bf16x8 zf = pad_tr_frag<4>(td, ra, ra + 8, 0);
 #pragma unroll
-      for (int ks = 0; ks < DQK / 16; ++ks) mma(sa[kb], swz_frag<T, KCPR>(tk, kb * 32 + n, 2 * ks + g), qf[ks]);
-#pragma unroll
-      for (int ks = 0; ks < DV / 16; ++ks)
-        mma(dp[kb], swz_frag<T, VCPR>(tv, kb * 32 + n, 2 * ks + g), swz_frag<T, VCPR>(sDO, wave * 32 + n, 2 * ks + g));
-    }
-    const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
-#pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float p = fast_exp2(__builtin_fmaf(sa[kb][r], P.scale_log2, -lse2));
-        if (need_mask) {
-          const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (key >= S || (P.causal && key > my_q)) p = 0.f;
-        }
-        dp[kb][r] = p * (dp[kb][r] - dlt);
+        for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], pad_tr_frag<KP>(tk, ra, ra + 8, db * 32), zf);
       }
-#pragma unroll
-    for (int kk = 0; kk < BC / 16; ++kk) {
-      const frag_t<T> zf = acc_to_frag<T>(dp[kk >> 1], kk & 1);
-      const int ra = kk * 16 + 4 * g;
-#pragma unroll
-      for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], swz_tr_frag<KCPR>(tk, ra, ra + 8, db * 32), zf);
     }
   };
-  for (int it = 0; it < ntiles; it += 2) {
+  for (int it = 0; it < ntiles; it += NS) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+    if (it + 2 < ntiles) step(std::integral_constant<int, 2>{}, it + 2);
+    if (it + 3 < ntiles) step(std::integral_constant<int, 3>{}, it + 3);
   }
 
-  if (my_q >= S) return;
+  const int my_q = t * 32 + n;
+  if (!wave_ok || my_q >= S) return;
   T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll
   for (int db = 0; db < DQK / 32; ++db)
@@ -307,10 +282,13 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   using Tl = BwdTiles<T>;
   constexpr int BR = 32 * Tl::WPH_Q;
   P.n_blocks = (P.S + BR - 1) / BR;
-  if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128)
-    dq_ring_kernel<DN, DR, DV, 32, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
-  else
+  if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
+    constexpr int WPH = 8;
+    P.n_blocks = (P.ds_T + WPH - 1) / WPH;
+    dq_ds_kernel<DN, DR, DV, WPH, 4><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
+  } else {
     dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
+  }
   return hipGetLastError();
 }
 

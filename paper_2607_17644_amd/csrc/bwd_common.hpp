@@ -37,7 +37,22 @@ struct BwdParams {
   int S, H, n_blocks;
   float scale, scale_log2;
   int causal;
+  // dS^T store (bf16 path with 192/128-wide heads): written by the key-stationary
+  // pass, read by the dQ pass; see ds_tile_offset. ds_T = ceil(S / 32).
+  void* ds;
+  int ds_T;
 };
+
+// dS^T store layout: for every (b, h) and query tile t of 32 rows, the keys that tile
+// sees (32 (t + 1) with the causal mask, 32 T without) as rows of 32 bf16 values, one
+// per query of the tile (key-major, 64-byte rows). Keys past S hold zeros.
+__host__ __device__ inline size_t ds_head_elems(int T, int causal) {
+  return causal ? (size_t)512 * T * (T + 1) : (size_t)1024 * T * T;
+}
+__host__ __device__ inline size_t ds_tile_offset(int T, int causal, int bh, int t) {
+  return (size_t)bh * ds_head_elems(T, causal) + (causal ? (size_t)512 * t * (t + 1) : (size_t)1024 * T * t);
+}
+__host__ __device__ inline int ds_tile_keys(int T, int causal, int t) { return causal ? 32 * (t + 1) : 32 * T; }
 
 template <typename T> struct BwdTiles;
 template <> struct BwdTiles<bf16> { static constexpr int BQ = 32, BC = 64, WPH_KV = 4, WPH_Q = 4; };

@@ -244,7 +244,8 @@ __device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_pt
 // model (checked exhaustively over chunk offsets and row blocks):
 //   16x16x32 operands (both patterns): P % 4 == 2 (CPR 16 -> 18, CPR 24 -> 26);
 //   32x32 16-byte row fragments only: P odd (CPR 8 -> 9, 16 -> 17, 24 -> 25);
-//   32x32 transposing reads only: P % 8 == 4 (CPR 16 -> 20, 24 -> 28);
+//   32x32 transposing reads only: P % 8 == 4 (CPR 16 -> 20, 24 -> 28), or P = 4 for
+//     tiles of exactly 32 columns (one 4-chunk group per row);
 // no pitch serves both 32x32 patterns; a tile read both ways keeps the XOR swizzle.
 //
 // Chunks to allocate for a padded tile: NROWS * P rounded up to whole wave
@@ -253,25 +254,48 @@ __host__ __device__ constexpr int pad_chunks(int nrows, int p) { return (nrows *
 
 // Direct global->LDS fill by NW waves: wave instruction j covers physical chunks
 // [64 j, 64 j + 64); lane i serves physical chunk p = 64 j + i, i.e. row p / P,
-// chunk p % P. Lanes on padding, or past the last row (the allocation is rounded up
-// to pad_chunks), reload chunk 0 of row 0 / of their row; those chunks are never read.
-template <typename T, int NROWS, int CPR, int P, int NW, typename RowPtr>
-__device__ __forceinline__ void pad_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+// chunk p % P, fetched from chunk_ptr(row, c). Lanes on padding, or past the last
+// row (the allocation, NCH chunks, is rounded up to whole instructions), reload chunk
+// 0 of their row / of row 0; those chunks are never read.
+template <typename T, int NROWS, int CPR, int P, int NW, int NCH = pad_chunks(NROWS, P), typename ChunkPtr>
+__device__ __forceinline__ void pad_fill_chunks(T* tile, int wave, int l, ChunkPtr chunk_ptr) {
   constexpr int E = 16 / sizeof(T);
-  constexpr int NI = pad_chunks(NROWS, P) / 64;
+  constexpr int NI = NCH / 64;
+  static_assert(NCH % 64 == 0 && NCH >= NROWS * P, "allocation must be whole instructions");
 #pragma unroll
   for (int j = wave; j < NI; j += NW) {
     const int p = j * 64 + l;
     int row = p / P, c = p % P;
     if (NI * 64 > NROWS * P && row >= NROWS) row = 0;
-    g2lds16(row_ptr(row) + (c < CPR ? c : 0) * E, tile + j * 64 * E);
+    g2lds16(chunk_ptr(row, c < CPR ? c : 0), tile + j * 64 * E);
   }
+}
+
+// Same, for tiles whose rows are contiguous in global memory: row_ptr(row) + 16 * c bytes.
+template <typename T, int NROWS, int CPR, int P, int NW, typename RowPtr>
+__device__ __forceinline__ void pad_fill(T* tile, int wave, int l, RowPtr row_ptr) {
+  constexpr int E = 16 / sizeof(T);
+  pad_fill_chunks<T, NROWS, CPR, P, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
 }
 
 // 16-byte row fragment: chunk c of `row` of a padded bf16 tile.
 template <int P>
 __device__ __forceinline__ bf16x8 pad_frag(const bf16* tile, int row, int c) {
   return *reinterpret_cast<const bf16x8*>(tile + (row * P + c) * 8);
+}
+
+// Transposing fragment (32x32x16 lane layout, see TrRead) from a padded bf16 tile of
+// pitch P chunks: lane l gets X[ra + e][c0 + l%32] and X[rb + e][c0 + l%32], e = 0..3.
+template <int P>
+__device__ __forceinline__ bf16x8 pad_tr_frag(const bf16* tile, int ra, int rb, int c0) {
+  const int l = threadIdx.x & 63, s = l & 15;
+  const int col = c0 + 16 * ((l >> 4) & 1) + 4 * (s & 3);
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const bf16* pa = tile + (ra + (s >> 2)) * P * 8 + col;
+  const bf16* pb = tile + (rb + (s >> 2)) * P * 8 + col;
+  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
+  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // Transposing fragment for the 16x16x32 shape from a padded bf16 tile: every 16-lane

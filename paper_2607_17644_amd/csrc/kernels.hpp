@@ -60,6 +60,7 @@ struct AttnBwdArgs {
   void* dkv;         // workspace [B,S,H,DN+DV]
   void* dkv_lo;      // workspace [B,S,H,DN+DV], bf16 only: dKV - bf16(dKV) rounded to bf16
   float* dkpe_h;     // workspace [B,S,H,DR]
+  void* ds;          // workspace: dS^T store (bf16 path with 192/128-wide heads), else unused
   int B, S, H;
   float scale;
   int causal;
