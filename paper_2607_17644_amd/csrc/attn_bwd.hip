@@ -23,6 +23,9 @@
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
 #include <type_traits>
 
+// direct global->LDS copies issued as inline assembly (exact LDS-read waits; the
+// rings order the copies with explicit waits and barriers)
+#define LAGA_LDS_DMA_ASM 1
 #include "common.hpp"
 #include "kernels.hpp"
 #include "bwd_common.hpp"
@@ -277,26 +280,39 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 // state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
 // the 32-key layout, so two waves share each SIMD and hide each other's latencies.
 // A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
-// stream through a two-stage LDS ring of direct global->LDS loads into padded tiles
-// (pitch = row + 2 chunks: conflict-free for both 16x16 read patterns, and every read
-// is a per-lane base address plus a constant, which keeps the kernel at ~200 VGPRs).
+// (Q, dO, and lse2 / delta of the rows) stream through an NS-stage LDS ring of direct
+// global->LDS loads into padded tiles (pitch = row + 2 chunks: conflict-free for both
+// 16x16 read patterns, and every read is a per-lane base address plus a constant).
 //   S = Q K^T, dP = dO V^T: A = Q / dO rows (16-byte row fragments), B = the lane's
 //       key / value row; accumulator: lane <-> key, 4 queries per 16-query block.
 //   dV^T += dO^T P, dK^T += Q^T dZ: the contraction over the tile's 32 queries takes
 //       P / dZ straight from the accumulators in the order {4G..4G+3, 16+4G..16+4G+3}
 //       (G = lane / 16), matched by two transposing 4-row reads of dO / Q.
-template <int DN, int DR, int DV, int WPH>
+// The loads of a tile form one list of instructions (Q chunks, dO chunks, one for the
+// lse2 / delta rows, padded with dummies to a multiple of the wave count), dealt out
+// round-robin, so every wave issues exactly KPW per tile: the wait before a tile then
+// counts loads exactly (loads complete in order; stores in between only make the wait
+// longer, never too short).
+template <int DN, int DR, int DV, int WPH, int NS>
 __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 16 * WPH;
   constexpr int QCPR = DQK / 8, OCPR = DV / 8;
   static_assert(QCPR % 4 == 0 && OCPR % 4 == 0, "padded pitches assume rows of whole 64-byte groups");
-  // two ring stages as distinct LDS objects (so the compiler does not make the reads
-  // of one stage wait for the direct loads into the other)
+  static_assert(NS >= 2 && NS <= 4, "ring depth");
   constexpr int QP = QCPR + 2, OP = OCPR + 2;  // pitches in chunks, P % 4 == 2
-  __shared__ __attribute__((aligned(16))) T sQ0[BQ * QP * 8], sQ1[BQ * QP * 8];
-  __shared__ __attribute__((aligned(16))) T sO0[BQ * OP * 8], sO1[BQ * OP * 8];
-  __shared__ __attribute__((aligned(16))) float sLD0[2 * BQ], sLD1[2 * BQ];  // lse2 then delta
+  constexpr int NQI = pad_chunks(BQ, QP) / 64, NOI = pad_chunks(BQ, OP) / 64;
+  constexpr int NLI = NQI + NOI;                // the lse2 / delta load
+  constexpr int KPW = (NLI + 1 + NW - 1) / NW;  // loads per wave per tile
+  static_assert(NQI * 64 == BQ * QP && NOI * 64 == BQ * OP, "tiles are whole load instructions");
+  // ring stages as distinct LDS objects (so the compiler does not make the reads of one
+  // stage wait for the direct loads into another); unused stages are not allocated
+  __shared__ __attribute__((aligned(16))) T sQ0[NQI * 512], sQ1[NQI * 512], sQ2[NQI * 512], sQ3[NQI * 512];
+  __shared__ __attribute__((aligned(16))) T sO0[NOI * 512], sO1[NOI * 512], sO2[NOI * 512], sO3[NOI * 512];
+  // lse2 of the tile's rows, then delta (the load instruction covers 1 KB; lanes 16..63
+  // repeat lanes 0..15)
+  __shared__ __attribute__((aligned(16))) float sL0[256], sL1[256], sL2[256], sL3[256];
+  __shared__ __attribute__((aligned(16))) T sDummy[512];  // target of the padding loads
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -310,7 +326,8 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   const int bh = lin / P.n_blocks;
   const int b = bh / H, h = bh % H;
 
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, j = l & 15, G = l >> 4;
+  const int tid = threadIdx.x, l = tid & 63, j = l & 15, G = l >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int k0 = kb * BK + wave * 16;
   const int my_k = k0 + j;
 
@@ -339,25 +356,44 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
   for (int i = 0; i < DV / 16; ++i) dv[i] = f32x4{};
 
-  const size_t hrow = (size_t)(b * H + h) * P.S_pad;
-  auto fill = [&](T* dq_, T* do_, float* dld, int qt) {
-    pad_fill<T, BQ, QCPR, QP, NW>(dq_, wave, l, [&](int r) {
-      return q + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DQK;
-    });
-    pad_fill<T, BQ, OCPR, OP, NW>(do_, wave, l, [&](int r) {
-      return dout + ((size_t)(b * S + min(qt + r, S - 1)) * H + h) * DV;
-    });
-    if (wave == NW - 1 && l < 2 * BQ / 4) {
-      const float* src = l < BQ / 4 ? P.lse2 + hrow + qt + 4 * l : P.delta + hrow + qt + 4 * (l - BQ / 4);
-      g2lds16(src, dld);
+  // this lane's chunk of each of the wave's loads: element offset from the tile's first
+  // row (Q / dO: row * row stride + chunk; lse2 / delta: 4 * index)
+  const float* lse2h = P.lse2 + (size_t)(b * H + h) * P.S_pad;
+  const float* deltah = P.delta + (size_t)(b * H + h) * P.S_pad;
+  auto chunk_of = [&](int js, int rmax, int& off) {  // js: instruction (wave-uniform)
+    if (js < NQI) {
+      const int p = js * 64 + l, r = min(p / QP, rmax), c = p % QP;
+      off = r * H * DQK + (c < QCPR ? c : 0) * 8;
+    } else if (js < NLI) {
+      const int p = (js - NQI) * 64 + l, r = min(p / OP, rmax), c = p % OP;
+      off = r * H * DV + (c < OCPR ? c : 0) * 8;
+    } else {
+      off = 4 * (j & 7);
+    }
+  };
+  int loff[KPW];
+#pragma unroll
+  for (int k = 0; k < KPW; ++k) chunk_of(wave + k * NW, BQ - 1, loff[k]);
+
+  auto fill = [&](T* tq, T* to, float* tl, int qt) {
+    const size_t row0 = (size_t)(b * S + qt) * H + h;
+    const bool tail = qt + BQ > S;  // rows past S are clamped to S-1 (their P is masked)
+#pragma unroll
+    for (int k = 0; k < KPW; ++k) {
+      const int js = wave + k * NW;
+      int off = loff[k];
+      if (tail && js < NLI) chunk_of(js, S - 1 - qt, off);
+      if (js < NQI) g2lds16(q + row0 * DQK + off, tq + js * 512);
+      else if (js < NLI) g2lds16(dout + row0 * DV + off, to + (js - NQI) * 512);
+      else if (js == NLI) g2lds16((j < 8 ? lse2h : deltah) + qt + off, tl);
+      else g2lds16(q + row0 * DQK, sDummy);
     }
   };
 
   // dS^T of a tile for the dQ pass: key my_k's row of 32 queries; the lane holds
   // queries {4G..4G+3} and {16+4G..16+4G+3}. Only the keys the tile sees are stored.
-  // The store of tile i is issued after the barrier of tile i + 1, ahead of that
-  // tile's loads, so the wait for those loads also covers it and its latency hides
-  // behind a whole tile (vector-memory stores and loads share one counter).
+  // The store of tile i is issued right after the barrier of tile i + 1, so its
+  // latency hides behind a whole tile.
   bf16x8 zs{};
   int ts = -1;
   auto store_ds = [&]() {
@@ -368,22 +404,47 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     }
   };
 
+  // live (query, key) pairs of this lane's key: q_lo <= query < q_lo + q_span (none
+  // for keys past S), tested with one unsigned compare
+  const int q_lo = P.causal ? my_k : 0;
+  const unsigned q_span = my_k < S ? (unsigned)(S - q_lo) : 0u;
+
   const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
   const int ntiles = (S - qt_begin + BQ - 1) / BQ;
-  fill(sQ0, sO0, sLD0, qt_begin);
+  auto stage_q = [&](auto st) -> T* {
+    constexpr int X = decltype(st)::value;
+    return X == 0 ? sQ0 : X == 1 ? sQ1 : X == 2 ? sQ2 : sQ3;
+  };
+  auto stage_o = [&](auto st) -> T* {
+    constexpr int X = decltype(st)::value;
+    return X == 0 ? sO0 : X == 1 ? sO1 : X == 2 ? sO2 : sO3;
+  };
+  auto stage_l = [&](auto st) -> float* {
+    constexpr int X = decltype(st)::value;
+    return X == 0 ? sL0 : X == 1 ? sL1 : X == 2 ? sL2 : sL3;
+  };
+  {
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    fill(stage_q(I0{}), stage_o(I0{}), stage_l(I0{}), qt_begin);
+    if (NS > 2 && ntiles > 1) fill(stage_q(I1{}), stage_o(I1{}), stage_l(I1{}), qt_begin + BQ);
+    if (NS > 3 && ntiles > 2) fill(stage_q(I2{}), stage_o(I2{}), stage_l(I2{}), qt_begin + 2 * BQ);
+  }
   auto step = [&](auto stage, int it) {
     constexpr int ST = decltype(stage)::value;
+    using NX = std::integral_constant<int, (ST + NS - 1) % NS>;
     const int qt = qt_begin + it * BQ;
-    wait_vmem();      // this wave's loads of tile `it` (and stores of tile it - 2) are done
-    __syncthreads();  // ... and everyone's; the other stage is free
+    // this wave's loads of tile `it` have landed: in the steady state exactly the
+    // NS - 2 later tiles' loads may still be in flight
+    if (NS > 2 && it >= NS - 2 && it + NS - 2 < ntiles) wait_vmem_le<(NS > 2 ? NS - 2 : 0) * KPW>();
+    else wait_vmem();
+    __syncthreads();  // ... and everyone's; the stage filled next (read at it - 1) is free
     store_ds();       // tile it - 1
-    if (it + 1 < ntiles) {
-      if constexpr (ST == 0) fill(sQ1, sO1, sLD1, qt + BQ);
-      else fill(sQ0, sO0, sLD0, qt + BQ);
-    }
-    const T* tq = ST == 0 ? sQ0 : sQ1;
-    const T* to = ST == 0 ? sO0 : sO1;
-    const float* tld = ST == 0 ? sLD0 : sLD1;
+    if (it + NS - 1 < ntiles) fill(stage_q(NX{}), stage_o(NX{}), stage_l(NX{}), qt + (NS - 1) * BQ);
+    const T* tq = stage_q(stage);
+    const T* to = stage_o(stage);
+    const float* tld = stage_l(stage);
     // masked: queries past S, keys past S (their dS is stored as zeros) and, causally,
     // keys after the query
     const bool need_mask = (P.causal && qt < k0 + 15) || (qt + BQ > S) || (k0 + 16 > S);
@@ -407,10 +468,7 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float p = fast_exp2(__builtin_fmaf(sa[qb][e], P.scale_log2, -lq[e]));
-        if (need_mask) {
-          const int qi = qt + qrow + e;
-          if (qi >= S || my_k >= S || (P.causal && my_k > qi)) p = 0.f;
-        }
+        if (need_mask) p = (unsigned)(qt + qrow + e - q_lo) < q_span ? p : 0.f;
         pf[qb * 4 + e] = to_elem<T>(p);
         zf[qb * 4 + e] = to_elem<T>(p * (dp[qb][e] - dq[e]));
       }
@@ -423,9 +481,11 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
     for (int db = 0; db < DQK / 16; ++db) mma16(dk[db], pad_tr_frag16<QP>(tq, ra, rb, db * 16), zf);
   };
-  for (int it = 0; it < ntiles; it += 2) {
+  for (int it = 0; it < ntiles; it += NS) {
     step(std::integral_constant<int, 0>{}, it);
-    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1 % NS>{}, it + 1);
+    if (NS > 2 && it + 2 < ntiles) step(std::integral_constant<int, 2 % NS>{}, it + 2);
+    if (NS > 3 && it + 3 < ntiles) step(std::integral_constant<int, 3 % NS>{}, it + 3);
   }
   store_ds();  // the last tile
 
@@ -489,9 +549,12 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
                                                       a.S, a.S_pad, a.H, BS);
   } else if (stage == 1) {
     if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
-      constexpr int WPH16 = 8, BK = 16 * WPH16;
+      // two stages: three and four measured 25 % and 17 % slower at S = 16384 (the
+      // loads are mostly cache hits that one tile of compute covers; more stages cost
+      // code size and scalar registers)
+      constexpr int WPH16 = 8, BK = 16 * WPH16, NS = 2;
       P.n_blocks = (a.S + BK - 1) / BK;
-      dkdv16_kernel<DN, DR, DV, WPH16><<<dim3(P.n_blocks * a.H, a.B), 64 * WPH16, 0, st>>>(P);
+      dkdv16_kernel<DN, DR, DV, WPH16, NS><<<dim3(P.n_blocks * a.H, a.B), 64 * WPH16, 0, st>>>(P);
     } else {
       constexpr int BK = 32 * Tl::WPH_KV;
       P.n_blocks = (a.S + BK - 1) / BK;

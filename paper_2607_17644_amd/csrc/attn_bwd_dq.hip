@@ -3,6 +3,9 @@
 // the recomputing kernel then needs no AGPR<->VGPR copies).
 #include <type_traits>
 
+// direct global->LDS copies issued as inline assembly (exact LDS-read waits; the
+// rings order the copies with explicit waits and barriers)
+#define LAGA_LDS_DMA_ASM 1
 #include "common.hpp"
 #include "kernels.hpp"
 #include "bwd_common.hpp"

@@ -88,13 +88,14 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
   // when some lane's max moved: the same arithmetic, in the same order, as the ring
   // kernel, so the two forward kernels agree bit for bit
   const bool need_mask = (causal && kt + BC - 1 > q0) || (kt + BC > S);
+  const int klim = causal ? min(S, my_q + 1) : S;  // live keys: key < klim
   if (need_mask) {
 #pragma unroll
     for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        if (key >= S || (causal && key > my_q)) sacc[kb][r] = -INFINITY;
+        sacc[kb][r] = key < klim ? sacc[kb][r] : -INFINITY;
       }
   }
   float mraw = -INFINITY;
@@ -352,13 +353,14 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
       }
     }
     const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
+    const int klim = P.causal ? min(S, my_q + 1) : S;  // live keys: key < klim
     if (need_mask) {
 #pragma unroll
       for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (key >= S || (P.causal && key > my_q)) sacc[kb][r] = -INFINITY;
+          sacc[kb][r] = key < klim ? sacc[kb][r] : -INFINITY;
         }
     }
     float mraw = -INFINITY;
@@ -638,7 +640,11 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * P.n_hgroups, a.B, 1);
   if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128 && Tl::G == 1) {
+#ifdef LAGA_FWD_OLD_RING
     attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, Tl::WPH><<<grid, 64 * Tl::WPH, 0, st>>>(P);
+#else
+    return launch_attn_fwd_pad(a, st);
+#endif
   } else {
     using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
     attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);

@@ -110,8 +110,28 @@ __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_lo
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
 // lane l's 16 bytes from `g` land at LDS address lds + 16 * l, where `lds` must be
 // the same for every lane of the wave. Tracked by vmcnt like any global load.
-__device__ __forceinline__ void g2lds16(const void* g, void* lds) {
+//
+// Two ways to issue it, chosen per source file with LAGA_LDS_DMA_ASM (defined before
+// this header is included):
+//   0: the compiler builtin. The compiler then models the copy as an access that may
+//      also count on the LGKM counter, after which it waits for every LDS read with
+//      lgkmcnt(0) (a full LDS round trip before each use).
+//   1: inline assembly the compiler does not see as a memory access of its own: LDS
+//      reads get exact lgkmcnt(N) waits. The kernel must then order the copies itself
+//      (an explicit vmcnt wait and a barrier before a stage is read or refilled),
+//      which every ring in this library does.
+#ifndef LAGA_LDS_DMA_ASM
+#define LAGA_LDS_DMA_ASM 0
+#endif
+// static: the definition differs between source files (see LAGA_LDS_DMA_ASM)
+static __device__ __forceinline__ void g2lds16(const void* g, void* lds) {
+#if LAGA_LDS_DMA_ASM
+  typedef __attribute__((address_space(3))) char lds_char;
+  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_char*)lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base) : "memory", "m0");
+#else
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+#endif
 }
 
 // Wait until all of this wave's outstanding vector-memory loads (including direct
@@ -277,6 +297,58 @@ __device__ __forceinline__ void pad_fill(T* tile, int wave, int l, RowPtr row_pt
   constexpr int E = 16 / sizeof(T);
   pad_fill_chunks<T, NROWS, CPR, P, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
 }
+
+// Padded-tile fill with the per-lane address arithmetic done once: the tile's rows
+// sit at a fixed element stride in global memory; chunks c < NSPLIT of row r come from
+// base0 + r * stride0 + 8 c, chunks c >= NSPLIT (if any) from base1 + r * stride1 +
+// 8 (c - NSPLIT). init() stores, for each of this wave's load instructions, the lane's
+// element offset (and which source it reads); fill() then costs one 64-bit add per
+// instruction. Only a tile that crosses the end of the data (rows_valid < NROWS) takes
+// the slower path that clamps rows to rows_valid - 1. Same chunk assignment as
+// pad_fill_chunks.
+template <typename T, int NROWS, int CPR, int P, int NW, int NSPLIT = CPR>
+struct PadFill {
+  static constexpr int E = 16 / sizeof(T);
+  static constexpr int NI = pad_chunks(NROWS, P) / 64;
+  static constexpr int K = (NI + NW - 1) / NW;  // most instructions any wave issues
+  int off[K];
+  int second;  // bit k: instruction k reads the second source
+  __device__ __forceinline__ void locate(int wave, int l, int k, int rmax, int& r, int& c) const {
+    const int p = (wave + k * NW) * 64 + l;
+    r = p / P;
+    c = p % P;
+    if (r >= NROWS) r = 0;
+    if (c >= CPR) c = 0;
+    r = min(r, rmax);
+  }
+  __device__ __forceinline__ void init(int wave, int l, int stride0, int stride1) {
+    second = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      int r, c;
+      locate(wave, l, k, NROWS - 1, r, c);
+      const bool s1 = c >= NSPLIT;
+      off[k] = s1 ? r * stride1 + (c - NSPLIT) * E : r * stride0 + c * E;
+      second |= (int)s1 << k;
+    }
+  }
+  __device__ __forceinline__ void fill(T* tile, int wave, int l, const T* base0, const T* base1, int stride0,
+                                       int stride1, int rows_valid) const {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int j = wave + k * NW;
+      if (j >= NI) break;  // wave-uniform
+      const bool s1 = (second >> k) & 1;
+      int o = off[k];
+      if (rows_valid < NROWS) {  // wave-uniform; the last tile only
+        int r, c;
+        locate(wave, l, k, rows_valid - 1, r, c);
+        o = s1 ? r * stride1 + (c - NSPLIT) * E : r * stride0 + c * E;
+      }
+      g2lds16((s1 ? base1 : base0) + o, tile + j * 64 * E);
+    }
+  }
+};
 
 // 16-byte row fragment: chunk c of `row` of a padded bf16 tile.
 template <int P>
