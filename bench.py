@@ -39,7 +39,118 @@ def parse():
                     help="heads of the workload the CPU oracle runs as its bounded sample")
     ap.add_argument("--fused-compare", action="store_true",
                     help="also time the forward with K/V rebuilt on chip (kv_mode=FUSED)")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: a plain copy kernel of known size (the HBM byte "
+                         "counters' calibration), then one warm-up and one measured step; prints nothing")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc output folders of --pmc-probe (FETCH_SIZE, then "
+                         "WRITE_SIZE) into the traffic summary under profiles/ and exit")
     return ap.parse_args()
+
+
+# HBM traffic of the dominant kernel, from counters (see --pmc-probe / --summarize-pmc).
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dkdv16_kernel_v3_train_s16384_hbm_traffic.txt")
+TRAFFIC_KERNEL = "dkdv16_kernel"
+COPY_BYTES = 1 << 30  # bytes read and bytes written by the calibration copy
+
+
+def kernel_fingerprint():
+    """Hash of the sources the dominant kernel is built from: stored traffic is only
+    reported while they are unchanged."""
+    import hashlib
+    hs = hashlib.sha256()
+    for f in ("attn_bwd.hip", "common.hpp", "bwd_common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2607_17644_amd", "csrc", f), "rb") as fh:
+            hs.update(fh.read())
+    return hs.hexdigest()[:16]
+
+
+def stored_traffic():
+    """Bytes per launch from the committed counter summary, or None if it is missing or
+    the kernel sources changed since the counters were taken."""
+    try:
+        kv = dict(line.strip().split("=", 1) for line in open(TRAFFIC_FILE) if "=" in line and not line.startswith("#"))
+    except OSError:
+        return None
+    if kv.get("fingerprint") != kernel_fingerprint():
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
+def summarize_pmc(fetch_dir, write_dir):
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rows += list(csv.DictReader(open(f)))
+        by_dispatch = {}
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            key = (r["Dispatch_Id"], r["Kernel_Name"])
+            by_dispatch[key] = by_dispatch.get(key, 0.0) + float(r["Counter_Value"])
+        out = {}
+        for (_, name), v in by_dispatch.items():
+            out.setdefault(name, []).append(v)
+        return out
+
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(d, sub):
+        ks = [k for k in d if sub in k]
+        if not ks:
+            raise SystemExit(f"no dispatch of {sub} in the counter output")
+        return ks[0], d[ks[0]]
+
+    def short(name):
+        import re
+        m = re.search(r"([A-Za-z_0-9]+)(<[^()]*>)?\(", name)
+        return m.group(1) if m else name[:60]
+
+    # calibration: the elementwise multiply (the copy of COPY_BYTES; the fill before it
+    # reads nothing)
+    cname, cf = pick(fetch, "MulFunctor")
+    _, cw = pick(write, "MulFunctor")
+    f_fetch = COPY_BYTES / (cf[0] * 1024.0)
+    f_write = COPY_BYTES / (cw[0] * 1024.0)
+    kname, kf = pick(fetch, TRAFFIC_KERNEL)
+    _, kw = pick(write, TRAFFIC_KERNEL)
+    kib_f, kib_w = kf[-1], kw[-1]  # the measured (last) step
+    bytes_launch = kib_f * 1024.0 * f_fetch + kib_w * 1024.0 * f_write
+    text = (
+        "# HBM traffic of the key-stationary backward kernel (one launch, workload v3_train_s16384),\n"
+        "# from two rocprofv3 --pmc runs of `python bench.py --pmc-probe` (FETCH_SIZE, then WRITE_SIZE),\n"
+        "# each scaled by what the same counter reads for a plain copy of 1 GiB (read 1 GiB, write 1 GiB).\n"
+        "# Commands (from the repository root):\n"
+        "#   rocprofv3 --pmc FETCH_SIZE --kernel-trace --output-format csv -d <F> -o p -- python bench.py --pmc-probe\n"
+        "#   rocprofv3 --pmc WRITE_SIZE --kernel-trace --output-format csv -d <W> -o p -- python bench.py --pmc-probe\n"
+        "#   python bench.py --summarize-pmc <F> <W>\n"
+        f"kernel={short(kname)}\n"
+        f"copy_kernel={short(cname)} (torch.mul of a 1 GiB fp32 tensor by 1)\n"
+        f"copy_fetch_kib={cf[0]:.1f}\ncopy_write_kib={cw[0]:.1f}\n"
+        f"fetch_scale={f_fetch:.4f}\nwrite_scale={f_write:.4f}\n"
+        f"fetch_kib_per_launch={kib_f:.1f}\nwrite_kib_per_launch={kib_w:.1f}\n"
+        f"hbm_bytes_per_launch={bytes_launch:.0f}\n"
+        f"fingerprint={kernel_fingerprint()}\n")
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
+def pmc_probe(w):
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1.0, out=dst)  # the calibration copy: reads and writes COPY_BYTES
+    torch.cuda.synchronize()
+    del src, dst
+    gpu_bench(w, 1, 1, False)
 
 
 def flops(w):
@@ -104,8 +215,12 @@ def gpu_bench(w, steps, warmup, fused_compare):
             parts[n].append(e[i].elapsed_time(e[i + 1]))
         parts["attn_bwd"].append(e[2].elapsed_time(e[len(names)]))
         parts["step"].append(e[0].elapsed_time(e[len(names)]))
+    def median(v):
+        v = sorted(v)
+        return v[len(v) // 2] if len(v) % 2 else 0.5 * (v[len(v) // 2 - 1] + v[len(v) // 2])
+    # per-part medians over the timed steps (the step total is the median of the totals)
     res = {"wall_ms_per_step": 1e3 * wall / steps,
-           "ms": {k: sum(v) / len(v) for k, v in parts.items()},
+           "ms": {k: median(v) for k, v in parts.items()},
            "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
     assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
 
@@ -156,6 +271,9 @@ def cpu_baseline(w, heads):
 
 def main():
     a = parse()
+    if a.summarize_pmc:
+        summarize_pmc(*a.summarize_pmc)
+        return
     if a.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the per-rank block has no "
                           "inter-GPU step (the collectives around it are out of scope); "
@@ -165,6 +283,9 @@ def main():
     w = LI.WORKLOADS[WORKLOAD]
     if a.seq_len:
         w = w.replace(seq_len=a.seq_len)
+    if a.pmc_probe:
+        pmc_probe(w)
+        return
     fl = flops(w)
     g = gpu_bench(w, a.steps, a.warmup, a.fused_compare)
     ms = g["ms"]["step"]
@@ -177,13 +298,16 @@ def main():
     pairs = float(w.batch) * S * S / 2 * H
     dkdv_flops = pairs * 2 * (2 * w.d_v + w.d_qk)
     achieved = dkdv_flops / (g["ms"]["bwd_dkdv"] * 1e-3) / 1e12
-    roofline = {"kernel": "dkdv_kernel", "bound": "mfma", "achieved": round(achieved, 1),
+    traffic = stored_traffic() if a.seq_len is None else None
+    roofline = {"kernel": TRAFFIC_KERNEL, "bound": "mfma", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None, "avg_launch_ms": round(g["ms"]["bwd_dkdv"], 4),
+                "traffic": None if traffic is None else round(traffic), "traffic_unit": "bytes per launch",
+                "avg_launch_ms": round(g["ms"]["bwd_dkdv"], 4),
                 "algorithmic_gflop_per_launch": round(dkdv_flops / 1e9, 1)}
     fwd_flops = 2 * pairs * (w.d_qk + w.d_v)
-    other = {"attn_fwd_kernel": round(fwd_flops / (g["ms"]["attn_fwd"] * 1e-3) / 1e12, 1),
-             "dq_kernel_dQ_only": round(pairs * 2 * w.d_qk / (g["ms"]["bwd_dq"] * 1e-3) / 1e12, 1)}
+    other = {"attn_fwd_ring_kernel": round(fwd_flops / (g["ms"]["attn_fwd"] * 1e-3) / 1e12, 1),
+             "dq_ds_kernel (dQ product)": round(pairs * 2 * w.d_qk / (g["ms"]["bwd_dq"] * 1e-3) / 1e12, 1),
+             "reconstruct GEMM": round(2.0 * w.batch * S * w.d_c * H * w.d_kvh / (g["ms"]["reconstruct_kv"] * 1e-3) / 1e12, 1)}
     cpu = None
     if not a.no_cpu_baseline:
         cpu = cpu_baseline(w, a.cpu_heads)

@@ -19,7 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblaga.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_fwd_pad.hip", "attn_bwd.hip", "attn_bwd_dq.hip"]
+SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -36,7 +36,6 @@ FLAGS = [
 # softmax / dZ arithmetic on the accumulators needs no AGPR<->VGPR copies).
 EXTRA = {
     "attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-    "attn_fwd_pad.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 

@@ -279,8 +279,12 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 // Key-stationary backward with 16 keys per wave on the 16x16x32 MFMA: the per-wave
 // state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
 // the 32-key layout, so two waves share each SIMD and hide each other's latencies.
+// (Measured alternatives, both slower at S = 16384: 32 keys per wave on the 32x32x16
+// MFMA at one wave per SIMD, 4.5 ms; a pair of waves splitting 32 keys by product
+// (S/P/dV on one, dP/dZ/dK on the other, P exchanged through LDS), 4.7 ms; this
+// kernel, 3.3 ms.)
 // A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
-// (Q, dO, and lse2 / delta of the rows) stream through an NS-stage LDS ring of direct
+// (Q, dO, and lse2 / delta of the rows) stream through a two-stage LDS ring of direct
 // global->LDS loads into padded tiles (pitch = row + 2 chunks: conflict-free for both
 // 16x16 read patterns, and every read is a per-lane base address plus a constant).
 //   S = Q K^T, dP = dO V^T: A = Q / dO rows (16-byte row fragments), B = the lane's
@@ -288,22 +292,16 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 //   dV^T += dO^T P, dK^T += Q^T dZ: the contraction over the tile's 32 queries takes
 //       P / dZ straight from the accumulators in the order {4G..4G+3, 16+4G..16+4G+3}
 //       (G = lane / 16), matched by two transposing 4-row reads of dO / Q.
-// The loads of a tile form one list of instructions (Q chunks, dO chunks, one for the
-// lse2 / delta rows, padded with dummies to a multiple of the wave count), dealt out
-// round-robin, so every wave issues exactly KPW per tile: the wait before a tile then
-// counts loads exactly (loads complete in order; stores in between only make the wait
-// longer, never too short).
+// Alongside, dS^T = dZ (bf16) is stored for the dQ pass.
 template <int DN, int DR, int DV, int WPH, int NS>
 __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 16 * WPH;
   constexpr int QCPR = DQK / 8, OCPR = DV / 8;
   static_assert(QCPR % 4 == 0 && OCPR % 4 == 0, "padded pitches assume rows of whole 64-byte groups");
-  static_assert(NS >= 2 && NS <= 4, "ring depth");
+  static_assert(NS == 2, "two-stage ring (the waits are full vmcnt waits)");
   constexpr int QP = QCPR + 2, OP = OCPR + 2;  // pitches in chunks, P % 4 == 2
   constexpr int NQI = pad_chunks(BQ, QP) / 64, NOI = pad_chunks(BQ, OP) / 64;
-  constexpr int NLI = NQI + NOI;                // the lse2 / delta load
-  constexpr int KPW = (NLI + 1 + NW - 1) / NW;  // loads per wave per tile
   static_assert(NQI * 64 == BQ * QP && NOI * 64 == BQ * OP, "tiles are whole load instructions");
   // ring stages as distinct LDS objects (so the compiler does not make the reads of one
   // stage wait for the direct loads into another); unused stages are not allocated
@@ -312,7 +310,6 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   // lse2 of the tile's rows, then delta (the load instruction covers 1 KB; lanes 16..63
   // repeat lanes 0..15)
   __shared__ __attribute__((aligned(16))) float sL0[256], sL1[256], sL2[256], sL3[256];
-  __shared__ __attribute__((aligned(16))) T sDummy[512];  // target of the padding loads
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -327,7 +324,7 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   const int b = bh / H, h = bh % H;
 
   const int tid = threadIdx.x, l = tid & 63, j = l & 15, G = l >> 4;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);  // uniform, known < NW
   const int k0 = kb * BK + wave * 16;
   const int my_k = k0 + j;
 
@@ -356,49 +353,62 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
   for (int i = 0; i < DV / 16; ++i) dv[i] = f32x4{};
 
-  // this lane's chunk of each of the wave's loads: element offset from the tile's first
-  // row (Q / dO: row * row stride + chunk; lse2 / delta: 4 * index)
-  const float* lse2h = P.lse2 + (size_t)(b * H + h) * P.S_pad;
-  const float* deltah = P.delta + (size_t)(b * H + h) * P.S_pad;
-  auto chunk_of = [&](int js, int rmax, int& off) {  // js: instruction (wave-uniform)
-    if (js < NQI) {
-      const int p = js * 64 + l, r = min(p / QP, rmax), c = p % QP;
-      off = r * H * DQK + (c < QCPR ? c : 0) * 8;
-    } else if (js < NLI) {
-      const int p = (js - NQI) * 64 + l, r = min(p / OP, rmax), c = p % OP;
-      off = r * H * DV + (c < OCPR ? c : 0) * 8;
-    } else {
-      off = 4 * (j & 7);
-    }
+  // Loads of a tile: Q chunks (instruction js of NQI goes to wave js % NW), dO chunks
+  // likewise, and the lse2 / delta rows in one instruction of wave NW - 1. Each lane
+  // keeps its source pointer for the tile at query 0, and a tile adds qt rows (one
+  // 64-bit add); which instructions a wave issues is fixed, so the dispatch is a few
+  // scalar compares. A tile crossing the end of the data (rows past S, clamped to
+  // S - 1; their P is masked) takes a slower path.
+  constexpr int KQ = (NQI + NW - 1) / NW, KO = (NOI + NW - 1) / NW;
+  auto q_chunk = [&](int js, int rmax) {  // element offset of this lane's Q chunk from row 0
+    const int p = js * 64 + l, r = min(p / QP, rmax), c = p % QP;
+    return r * H * DQK + (c < QCPR ? c : 0) * 8;
   };
-  int loff[KPW];
+  auto o_chunk = [&](int js, int rmax) {
+    const int p = js * 64 + l, r = min(p / OP, rmax), c = p % OP;
+    return r * H * DV + (c < OCPR ? c : 0) * 8;
+  };
+  const size_t hrow0 = (size_t)(b * S) * H + h;  // row (b, 0, h)
+  const T* qlane[KQ];
+  const T* olane[KO];
 #pragma unroll
-  for (int k = 0; k < KPW; ++k) chunk_of(wave + k * NW, BQ - 1, loff[k]);
+  for (int k = 0; k < KQ; ++k) qlane[k] = q + hrow0 * DQK + q_chunk(wave + k * NW, BQ - 1);
+#pragma unroll
+  for (int k = 0; k < KO; ++k) olane[k] = dout + hrow0 * DV + o_chunk(wave + k * NW, BQ - 1);
+  const float* llane = (j < 8 ? P.lse2 : P.delta) + (size_t)(b * H + h) * P.S_pad + 4 * (j & 7);
 
   auto fill = [&](T* tq, T* to, float* tl, int qt) {
-    const size_t row0 = (size_t)(b * S + qt) * H + h;
-    const bool tail = qt + BQ > S;  // rows past S are clamped to S-1 (their P is masked)
+    const size_t qstep = (size_t)qt * H;
+    if (qt + BQ <= S) {
 #pragma unroll
-    for (int k = 0; k < KPW; ++k) {
-      const int js = wave + k * NW;
-      int off = loff[k];
-      if (tail && js < NLI) chunk_of(js, S - 1 - qt, off);
-      if (js < NQI) g2lds16(q + row0 * DQK + off, tq + js * 512);
-      else if (js < NLI) g2lds16(dout + row0 * DV + off, to + (js - NQI) * 512);
-      else if (js == NLI) g2lds16((j < 8 ? lse2h : deltah) + qt + off, tl);
-      else g2lds16(q + row0 * DQK, sDummy);
+      for (int k = 0; k < KQ; ++k)
+        if (wave + k * NW < NQI) g2lds16(qlane[k] + qstep * DQK, tq + (wave + k * NW) * 512);
+#pragma unroll
+      for (int k = 0; k < KO; ++k)
+        if (wave + k * NW < NOI) g2lds16(olane[k] + qstep * DV, to + (wave + k * NW) * 512);
+    } else {
+      const T* qb = q + (hrow0 + qstep) * DQK;
+      const T* ob = dout + (hrow0 + qstep) * DV;
+#pragma unroll
+      for (int k = 0; k < KQ; ++k)
+        if (wave + k * NW < NQI) g2lds16(qb + q_chunk(wave + k * NW, S - 1 - qt), tq + (wave + k * NW) * 512);
+#pragma unroll
+      for (int k = 0; k < KO; ++k)
+        if (wave + k * NW < NOI) g2lds16(ob + o_chunk(wave + k * NW, S - 1 - qt), to + (wave + k * NW) * 512);
     }
+    if (wave == NW - 1) g2lds16(llane + qt, tl);
   };
 
   // dS^T of a tile for the dQ pass: key my_k's row of 32 queries; the lane holds
   // queries {4G..4G+3} and {16+4G..16+4G+3}. Only the keys the tile sees are stored.
   // The store of tile i is issued right after the barrier of tile i + 1, so its
-  // latency hides behind a whole tile.
+  // latency hides behind a whole tile. dsl: this key's row in query tile 0.
+  T* const dsl = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, 0) + (size_t)my_k * BQ;
   bf16x8 zs{};
   int ts = -1;
   auto store_ds = [&]() {
     if (ts >= 0 && my_k < ds_tile_keys(P.ds_T, P.causal, ts)) {
-      T* dsr = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, ts) + (size_t)my_k * BQ;
+      T* dsr = dsl + (P.causal ? (size_t)512 * ts * (ts + 1) : (size_t)1024 * P.ds_T * ts);
       *reinterpret_cast<bf16x4*>(dsr + 4 * G) = __builtin_shufflevector(zs, zs, 0, 1, 2, 3);
       *reinterpret_cast<bf16x4*>(dsr + 16 + 4 * G) = __builtin_shufflevector(zs, zs, 4, 5, 6, 7);
     }
@@ -437,8 +447,7 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
     const int qt = qt_begin + it * BQ;
     // this wave's loads of tile `it` have landed: in the steady state exactly the
     // NS - 2 later tiles' loads may still be in flight
-    if (NS > 2 && it >= NS - 2 && it + NS - 2 < ntiles) wait_vmem_le<(NS > 2 ? NS - 2 : 0) * KPW>();
-    else wait_vmem();
+    wait_vmem();
     __syncthreads();  // ... and everyone's; the stage filled next (read at it - 1) is free
     store_ds();       // tile it - 1
     if (it + NS - 1 < ntiles) fill(stage_q(NX{}), stage_o(NX{}), stage_l(NX{}), qt + (NS - 1) * BQ);
@@ -459,6 +468,14 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
       for (int ks = 0; ks < DV / 32; ++ks) mma16(dp[qb], pad_frag<OP>(to, qb * 16 + j, 4 * ks + G), vf[ks]);
     }
+    if (need_mask) {
+      asm volatile("");  // keep the branch: the common unmasked tile runs no mask code
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          sa[qb][e] = (unsigned)(qt + qb * 16 + G * 4 + e - q_lo) < q_span ? sa[qb][e] : -INFINITY;
+    }
     bf16x8 pf, zf;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -468,7 +485,6 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float p = fast_exp2(__builtin_fmaf(sa[qb][e], P.scale_log2, -lq[e]));
-        if (need_mask) p = (unsigned)(qt + qrow + e - q_lo) < q_span ? p : 0.f;
         pf[qb * 4 + e] = to_elem<T>(p);
         zf[qb * 4 + e] = to_elem<T>(p * (dp[qb][e] - dq[e]));
       }

@@ -88,15 +88,15 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
   // when some lane's max moved: the same arithmetic, in the same order, as the ring
   // kernel, so the two forward kernels agree bit for bit
   const bool need_mask = (causal && kt + BC - 1 > q0) || (kt + BC > S);
-  const int klim = causal ? min(S, my_q + 1) : S;  // live keys: key < klim
   if (need_mask) {
+    asm volatile("");  // keep the branch (see the ring kernel)
+    // live keys: key < klim, i.e. accumulator row (r/4)*8 + r%4 + 32 kb < klim - kt - 4 g
+    const int lim = (causal ? min(S, my_q + 1) : S) - kt - 4 * g;
 #pragma unroll
     for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        sacc[kb][r] = key < klim ? sacc[kb][r] : -INFINITY;
-      }
+      for (int r = 0; r < 16; ++r)
+        sacc[kb][r] = kb * 32 + (r >> 2) * 8 + (r & 3) < lim ? sacc[kb][r] : -INFINITY;
   }
   float mraw = -INFINITY;
 #pragma unroll
@@ -105,8 +105,13 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
     for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[kb][r]);
   mraw = wave_xor32_max(mraw);
   const float m_new = fmaxf(m, mraw * scale_log2);
-  const float m_use = m_new == -INFINITY ? 0.f : m_new;
-  const float alpha = fast_exp2(m - m_use);
+  // lazy rescale: the reference max m moves only when a score exceeds it by more
+  // than 2^kRescaleLog2 (until then p <= 2^kRescaleLog2), so O^T is rarely rescaled;
+  // the normalised result is the same
+  const bool bump = m_new > m + kRescaleLog2;
+  const float m_ref = bump ? m_new : m;
+  const float alpha = bump ? fast_exp2(m - m_new) : 1.f;
+  const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
   float ps = 0.f;
 #pragma unroll
   for (int kb = 0; kb < BC / 32; ++kb)
@@ -117,8 +122,8 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
       ps += p;
     }
   lsum = lsum * alpha + ps;
-  m = m_new;
-  if (__ballot(alpha != 1.f)) {
+  m = m_ref;
+  if (__ballot(bump)) {
 #pragma unroll
     for (int i = 0; i < DV / 32; ++i) oacc[i] *= alpha;
   }
@@ -293,7 +298,8 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   const int bh = lin / P.n_qblocks;
   const int b = bh / H, h = bh % H;
 
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
+  const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q0 = qb * BR + wave * 32;
   const int my_q = q0 + n;
   const int kend = P.causal ? min(S, (qb + 1) * BR) : S;
@@ -313,17 +319,17 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   for (int i = 0; i < DV / 32; ++i) oacc[i] = f32x16{};
   float m = -INFINITY, lsum = 0.f;
 
+  // key rows past S are clamped to S-1 (valid memory) and masked below
+  SwzRowFill<T, BC, KCPR, NW> kfill, vfill;
+  SwzRowFill<T, BC, PCPR, NW> pfill;
+  kfill.init(wave, l, H * DKVH);
+  vfill.init(wave, l, H * DKVH);
+  pfill.init(wave, l, DR);
   auto fill = [&](T* dk, T* dp, T* dv, int kt) {
-    // key rows past S are clamped to S-1 (valid memory) and masked below
-    swz_fill<T, BC, KCPR, NW>(dk, wave, l, [&](int r) {
-      return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH;
-    });
-    swz_fill<T, BC, VCPR, NW>(dv, wave, l, [&](int r) {
-      return kv + ((size_t)(b * S + min(kt + r, S - 1)) * H + h) * DKVH + DN;
-    });
-    swz_fill<T, BC, PCPR, NW>(dp, wave, l, [&](int r) {
-      return kpe + (size_t)(b * S + min(kt + r, S - 1)) * DR;
-    });
+    const T* kvb = kv + ((size_t)(b * S + kt) * H + h) * DKVH;
+    kfill.fill(dk, wave, l, kvb, H * DKVH, S - kt);
+    vfill.fill(dv, wave, l, kvb + DN, H * DKVH, S - kt);
+    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, S - kt);
   };
 
   const int ntiles = (kend + BC - 1) / BC;
@@ -337,6 +343,7 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
       if constexpr (ST == 0) fill(sK1, sP1, sV1, kt + BC);
       else fill(sK0, sP0, sV0, kt + BC);
     }
+    if (P.causal && kt > q0 + 31) return;  // wave-uniform: every key of the tile is masked for this wave
     const T* tk = ST == 0 ? sK0 : sK1;
     const T* tp = ST == 0 ? sP0 : sP1;
     const T* tv = ST == 0 ? sV0 : sV1;
@@ -353,15 +360,17 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
       }
     }
     const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
-    const int klim = P.causal ? min(S, my_q + 1) : S;  // live keys: key < klim
     if (need_mask) {
+      // the empty volatile statement keeps this a real branch (if-converted, the mask
+      // would cost every tile two VALU operations per score)
+      asm volatile("");
+      // live keys: key < klim, i.e. accumulator row (r/4)*8 + r%4 + 32 kb < klim - kt - 4 g
+      const int lim = (P.causal ? min(S, my_q + 1) : S) - kt - 4 * g;
 #pragma unroll
       for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          sacc[kb][r] = key < klim ? sacc[kb][r] : -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          sacc[kb][r] = kb * 32 + (r >> 2) * 8 + (r & 3) < lim ? sacc[kb][r] : -INFINITY;
     }
     float mraw = -INFINITY;
 #pragma unroll
@@ -370,8 +379,13 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
       for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[kb][r]);
     mraw = wave_xor32_max(mraw);
     const float m_new = fmaxf(m, mraw * P.scale_log2);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m - m_use);
+    // lazy rescale: the reference max m moves only when a score exceeds it by more
+    // than 2^kRescaleLog2 (until then p <= 2^kRescaleLog2), so O^T is rarely rescaled;
+    // the normalised result is the same
+    const bool bump = m_new > m + kRescaleLog2;
+    const float m_ref = bump ? m_new : m;
+    const float alpha = bump ? fast_exp2(m - m_new) : 1.f;
+    const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
     float ps = 0.f;
 #pragma unroll
     for (int kb = 0; kb < BC / 32; ++kb)
@@ -382,8 +396,8 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
         ps += p;
       }
     lsum = lsum * alpha + ps;
-    m = m_new;
-    if (__ballot(alpha != 1.f)) {
+    m = m_ref;
+    if (__ballot(bump)) {
 #pragma unroll
       for (int i = 0; i < DV / 32; ++i) oacc[i] *= alpha;
     }
@@ -640,11 +654,11 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * P.n_hgroups, a.B, 1);
   if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128 && Tl::G == 1) {
-#ifdef LAGA_FWD_OLD_RING
-    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, Tl::WPH><<<grid, 64 * Tl::WPH, 0, st>>>(P);
-#else
-    return launch_attn_fwd_pad(a, st);
-#endif
+    // 8 waves: 256 queries of one head per workgroup, which halves the K/V tile
+    // traffic of 4 waves (measured 8 % faster at S = 16384)
+    constexpr int RW = 8, RBR = 32 * RW;
+    P.n_qblocks = (a.S + RBR - 1) / RBR;
+    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, RW><<<dim3(P.n_qblocks * P.n_hgroups, a.B, 1), 64 * RW, 0, st>>>(P);
   } else {
     using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
     attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);

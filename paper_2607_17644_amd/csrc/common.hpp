@@ -126,8 +126,9 @@ __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_lo
 // static: the definition differs between source files (see LAGA_LDS_DMA_ASM)
 static __device__ __forceinline__ void g2lds16(const void* g, void* lds) {
 #if LAGA_LDS_DMA_ASM
-  typedef __attribute__((address_space(3))) char lds_char;
-  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_char*)lds);
+  // the low 32 bits of a generic pointer into LDS are its LDS address (an address
+  // space cast would add a null check)
+  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base) : "memory", "m0");
 #else
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
@@ -385,6 +386,37 @@ __device__ __forceinline__ bf16x8 pad_tr_frag16(const bf16* tile, int ra, int rb
   bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
+
+// Swizzled-tile fill with the per-lane address arithmetic hoisted. For CPR = 8 or 16 a
+// load instruction covers 64 / CPR whole rows, and the swizzle depends on the row bits
+// that the instruction index sets only through its residue modulo 2 (CPR 8) or 4
+// (CPR 16); with NW a multiple of that, a lane's chunk permutation is the same in
+// every instruction of its wave. So init() computes one element offset per lane, and
+// a fill adds a wave-uniform row offset per instruction. Rows sit at a fixed element
+// stride in global memory; a tile that crosses the end of the data (rows_valid <
+// NROWS) takes the general path, clamping rows to rows_valid - 1.
+template <typename T, int NROWS, int CPR, int NW>
+struct SwzRowFill {
+  static_assert(CPR == 8 || CPR == 16, "whole rows per load instruction");
+  static constexpr int E = 16 / sizeof(T), RPI = 64 / CPR, NI = NROWS * CPR / 64;
+  static_assert(NI * 64 == NROWS * CPR && NW % (CPR == 16 ? 4 : 2) == 0, "uniform chunk permutation per wave");
+  int lane_off;
+  __device__ __forceinline__ void init(int wave, int l, int stride) {
+    const int rl = l / CPR;
+    lane_off = rl * stride + ((l % CPR) ^ swz<CPR>(RPI * wave + rl)) * E;
+  }
+  __device__ __forceinline__ void fill(T* tile, int wave, int l, const T* base, int stride, int rows_valid) const {
+#pragma unroll
+    for (int j = wave; j < NI; j += NW) {
+      if (rows_valid >= NROWS) {
+        g2lds16(base + j * RPI * stride + lane_off, tile + j * 64 * E);
+      } else {
+        const int row = j * RPI + l / CPR, c = (l % CPR) ^ swz<CPR>(row);
+        g2lds16(base + min(row, rows_valid - 1) * stride + c * E, tile + j * 64 * E);
+      }
+    }
+  }
+};
 
 // Zero value of a 16-byte staging chunk.
 __device__ __forceinline__ chunk16 zero_chunk() { chunk16 z = {0, 0, 0, 0}; return z; }

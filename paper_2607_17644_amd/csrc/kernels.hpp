@@ -36,10 +36,13 @@ struct AttnFwdArgs {
   int causal;
 };
 
+// Online softmax of the forward kernels: the running reference max is only raised
+// when a new score exceeds it by more than this (log2 units), so unnormalised
+// probabilities stay <= 2^kRescaleLog2 and the O^T rescale is rare.
+constexpr float kRescaleLog2 = 8.f;
+
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
-// bf16, 128/64/128-wide heads, materialised K/V (attn_fwd_pad.hip).
-hipError_t launch_attn_fwd_pad(const AttnFwdArgs& a, hipStream_t st);
 
 // Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T
 // (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
