@@ -52,7 +52,7 @@ size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ?
 
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | dW split partials |
+// Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | GEMM split partials |
 // kv rebuild | dS^T store (bf16 with 192/128-wide heads)]
 struct BwdWs {
   size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, ds, total;
@@ -68,8 +68,8 @@ BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   w.dkv = off; off += round_up(elem_size(p) * tok * d.H * d.dkvh());
   w.dkv_lo = off; off += p->dtype == LAGA_DTYPE_BF16 ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
   w.dkpe_h = off; off += round_up(sizeof(float) * tok * d.H * d.dr);
-  const size_t ns = dw_split_count((int)tok);
-  w.dw_part = off; off += ns > 1 ? round_up(sizeof(float) * ns * d.d_c * d.H * d.dkvh()) : 0;
+  const size_t np = gemm_partial_elems((int)tok, d.d_c, d.H * d.dkvh());
+  w.dw_part = off; off += np > 0 ? round_up(sizeof(float) * np) : 0;
   w.kv = off; off += p->kv_mode == LAGA_KV_FUSED ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
   w.ds = off;
   off += stores_ds(p) ? round_up(sizeof(uint16_t) * (size_t)d.B * d.H * bwd::ds_head_elems((d.S + 31) / 32, p->causal)) : 0;
@@ -212,11 +212,11 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
   if (bf) {
     const bf16* hi = (const bf16*)a.dkv;
     const bf16* lo = (const bf16*)a.dkv_lo;
-    e = launch_dc<bf16>(hi, lo, (const bf16*)w_kv_b, dc_kv, tok, d.d_c, ncol, st);
+    e = launch_dc<bf16>(hi, lo, (const bf16*)w_kv_b, dc_kv, part, tok, d.d_c, ncol, st);
     if (e == hipSuccess) e = launch_dw<bf16>((const bf16*)c_kv, hi, lo, dw_kv_b, part, d.d_c, ncol, tok, st);
   } else {
     const float* g = (const float*)a.dkv;
-    e = launch_dc<float>(g, nullptr, (const float*)w_kv_b, dc_kv, tok, d.d_c, ncol, st);
+    e = launch_dc<float>(g, nullptr, (const float*)w_kv_b, dc_kv, part, tok, d.d_c, ncol, st);
     if (e == hipSuccess) e = launch_dw<float>((const float*)c_kv, g, nullptr, dw_kv_b, part, d.d_c, ncol, tok, st);
   }
   return from_hip(e);

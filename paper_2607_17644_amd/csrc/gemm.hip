@@ -13,9 +13,10 @@
 // lane's accumulators for vectorised stores.
 //
 // Per output element the contraction runs over K in ascending 16-wide steps
-// (one MFMA each) with fp32 accumulation; tile shapes and the split size do not
-// depend on N, so a column of the output is bit-identical whatever N (the
-// number of heads) is.
+// (one MFMA each) with fp32 accumulation; tile shapes and the dW token split do
+// not depend on N, so a column of the output is bit-identical whatever N (the
+// number of heads) is. (dc_kv's contraction runs over the heads and may be split
+// into partials summed in a fixed order.)
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -223,36 +224,71 @@ hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, int M, int N, int K, hipStream_t st) {
-  // dc[M=tokens][N=d_c] = (dKV + dKV_lo)[M][K=H*dkvh] @ W^T ; W stored [N][K] (k-contiguous).
-  using G = GemmCfg<T>;
-  dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, 1);
-  if (dkv_lo)
-    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 1><<<grid, kThreads, 0, st>>>(
-        dkv, w, dkv_lo, dc, M, N, K, K, K, N, K, 0);
-  else
-    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
-        dkv, w, nullptr, dc, M, N, K, K, K, N, K, 0);
-  return hipGetLastError();
+namespace {
+constexpr int kMinGemmBlocks = 512;  // workgroups wanted per GEMM launch (256 CUs)
+}  // namespace
+
+int dw_split_tokens(int tokens) {
+  int s = 2048;
+  while (s > 512 && (tokens + s - 1) / s < 4) s /= 2;
+  return s;
+}
+size_t dw_split_count(int tokens) {
+  const int s = dw_split_tokens(tokens);
+  return (size_t)((tokens + s - 1) / s);
+}
+int dc_split_count(int tokens, int d_c, int K) {
+  const int tiles = grid_tiles(tokens, d_c, GemmCfg<bf16>::BM, GemmCfg<bf16>::BN);
+  const int max_split = K / 256;  // at least one head (256 contraction indices) per split
+  int n = (kMinGemmBlocks + tiles - 1) / tiles;
+  return n < 1 ? 1 : (n > max_split ? max_split : n);
+}
+size_t gemm_partial_elems(int tokens, int d_c, int K) {
+  const size_t dw = dw_split_count(tokens) > 1 ? dw_split_count(tokens) * (size_t)d_c * K : 0;
+  const int ndc = dc_split_count(tokens, d_c, K);
+  const size_t dc = ndc > 1 ? (size_t)ndc * tokens * d_c : 0;
+  return dw > dc ? dw : dc;
 }
 
-size_t dw_split_count(int tokens) { return (size_t)((tokens + kDwSplitTokens - 1) / kDwSplitTokens); }
+template <typename T>
+hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, float* partial, int M, int N, int K,
+                     hipStream_t st) {
+  // dc[M=tokens][N=d_c] = (dKV + dKV_lo)[M][K=H*dkvh] @ W^T ; W stored [N][K] (k-contiguous).
+  // With a split contraction each split writes its partial and a fixed-order reduce sums them.
+  using G = GemmCfg<T>;
+  const int nsplit = sizeof(T) == 2 ? dc_split_count(M, N, K) : 1;
+  const int k_chunk = (K / nsplit + G::BK - 1) / G::BK * G::BK;
+  const int nz = (K + k_chunk - 1) / k_chunk;
+  float* target = nz == 1 ? dc : partial;
+  dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, nz);
+  if (dkv_lo)
+    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 1><<<grid, kThreads, 0, st>>>(
+        dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
+  else
+    gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
+        dkv, w, nullptr, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
+  if (nz > 1) {
+    const long long n4 = (long long)M * N / 4;
+    split_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(partial, dc, n4, nz, (long long)M * N);
+  }
+  return hipGetLastError();
+}
 
 template <typename T>
 hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float* partial, int M, int N, int K,
                      hipStream_t st) {
   // dW[M=d_c][N=H*dkvh] = c^T @ (dKV + dKV_lo); c stored [K=tokens][M] and dKV [K][N]: both k-strided.
   using G = GemmCfg<T>;
+  const int split = dw_split_tokens(K);
   const int nsplit = (int)dw_split_count(K);
   float* target = nsplit == 1 ? dw : partial;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, nsplit);
   if (dkv_lo)
     gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 2><<<grid, kThreads, 0, st>>>(
-        c, dkv, dkv_lo, target, M, N, K, M, N, N, kDwSplitTokens, (long long)M * N);
+        c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
   else
     gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
-        c, dkv, nullptr, target, M, N, K, M, N, N, kDwSplitTokens, (long long)M * N);
+        c, dkv, nullptr, target, M, N, K, M, N, N, split, (long long)M * N);
   if (nsplit > 1) {
     const long long n4 = (long long)M * N / 4;
     split_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(partial, dw, n4, nsplit, (long long)M * N);
@@ -262,8 +298,9 @@ hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float
 
 template hipError_t launch_reconstruct<bf16>(const bf16*, const bf16*, bf16*, int, int, int, hipStream_t);
 template hipError_t launch_reconstruct<float>(const float*, const float*, float*, int, int, int, hipStream_t);
-template hipError_t launch_dc<bf16>(const bf16*, const bf16*, const bf16*, float*, int, int, int, hipStream_t);
-template hipError_t launch_dc<float>(const float*, const float*, const float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dc<bf16>(const bf16*, const bf16*, const bf16*, float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_dc<float>(const float*, const float*, const float*, float*, float*, int, int, int,
+                                     hipStream_t);
 template hipError_t launch_dw<bf16>(const bf16*, const bf16*, const bf16*, float*, float*, int, int, int, hipStream_t);
 template hipError_t launch_dw<float>(const float*, const float*, const float*, float*, float*, int, int, int,
                                      hipStream_t);

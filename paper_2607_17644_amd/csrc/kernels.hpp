@@ -10,15 +10,24 @@ namespace laga {
 // multiple of this many queries, so query tiles can be fetched whole.
 constexpr int kRowPad = 64;
 
-// Tokens per split of the dW reduction (fixed: never depends on the head count).
-constexpr int kDwSplitTokens = 2048;
+// Tokens per split of the dW reduction over tokens: a function of the token count only
+// (never of the head count), so each dW column is bit-identical whatever head shard
+// computes it. 2048 for long sequences, down to 512 for short ones (enough workgroups).
+int dw_split_tokens(int tokens);
 size_t dw_split_count(int tokens);
+// Splits of the dc_kv GEMM's contraction (over the shard's heads x 256), chosen so that
+// the launch has enough workgroups; dc_kv sums over heads, so no bit-identity across
+// head shards is asked of it. Partials of both GEMMs share one workspace buffer.
+int dc_split_count(int tokens, int d_c, int K);
+size_t gemm_partial_elems(int tokens, int d_c, int K);
 
 template <typename T>
 hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st);
 // dkv_lo (may be NULL): low bf16 halves of dKV, so that dKV = dkv + dkv_lo to ~16 bits.
+// partial: workspace of gemm_partial_elems floats (used when the contraction is split).
 template <typename T>
-hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, int M, int N, int K, hipStream_t st);
+hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, float* partial, int M, int N, int K,
+                     hipStream_t st);
 template <typename T>
 hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float* partial, int M, int N, int K,
                      hipStream_t st);
