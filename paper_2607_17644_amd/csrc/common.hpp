@@ -96,6 +96,15 @@ __device__ __forceinline__ frag_t<T> acc_to_frag(const f32x16& acc, int half) {
   for (int e = 0; e < 8; ++e) f[e] = to_elem<T>(acc[8 * half + e]);
   return f;
 }
+// bf16: one vector conversion, so that pairs map onto packed RNE conversions
+template <>
+__device__ __forceinline__ frag_t<bf16> acc_to_frag<bf16>(const f32x16& acc, int half) {
+  typedef float f32x8 __attribute__((ext_vector_type(8)));
+  f32x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = acc[8 * half + e];
+  return __builtin_convertvector(v, bf16x8);
+}
 
 __device__ __forceinline__ float wave_xor32_max(float x) {
   return fmaxf(x, __shfl_xor(x, 32));
@@ -133,6 +142,25 @@ static __device__ __forceinline__ void g2lds16(const void* g, void* lds) {
 #else
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 #endif
+}
+
+// The same copy from a wave-uniform base plus a per-lane 32-bit byte offset (the
+// scalar-base addressing form: one VGPR per lane instead of a 64-bit address).
+#if LAGA_LDS_DMA_ASM
+static __device__ __forceinline__ void g2lds16_so(const void* base, uint32_t off, void* lds) {
+  const uint32_t m = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(m)
+               : "memory", "m0");
+}
+#endif
+
+// Workgroup barrier ordering LDS only: waits for this wave's LDS accesses, not for
+// its global stores (__syncthreads also waits until every global store of the wave
+// has completed). Direct global->LDS copies still need their own vmcnt wait first.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // Wait until all of this wave's outstanding vector-memory loads (including direct

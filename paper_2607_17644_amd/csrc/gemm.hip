@@ -17,6 +17,9 @@
 // not depend on N, so a column of the output is bit-identical whatever N (the
 // number of heads) is. (dc_kv's contraction runs over the heads and may be split
 // into partials summed in a fixed order.)
+// direct global->LDS copies issued as inline assembly (exact LDS-read waits; the
+// ring orders the copies with explicit waits and barriers)
+#define LAGA_LDS_DMA_ASM 1
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -194,6 +197,241 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
     }
 }
 
+// ------------------------------------------------------------------ large tiles (bf16)
+// A workgroup of four waves computes a BM x BN output tile (BM * BN = 4 * 128 * 128),
+// one wave per SIMD, each wave 128 x 128 (4 x 4 blocks of 32 x 32, 256 accumulator
+// registers per lane): an LDS operand fragment then feeds four MFMAs, so LDS reads
+// stay well under the LDS rate. Besides 256 x 256, 128 x 512 and 512 x 128 tiles cover
+// a whole 512-wide side, so the other (large) operand is read from memory once.
+// The contraction advances 32 at a time through an LDS ring of NSLOT stages filled by
+// direct global->LDS copies issued NSLOT - 1 stages ahead (a stage of MFMAs is shorter
+// than the latency of a load from memory); one barrier per stage, placed inside the
+// second half of the stage's MFMAs, with the next stage's first operands read before
+// the last MFMAs.
+//
+// Operand tiles are ROWS (the non-contraction index) x 32 contraction indices, stored
+// unpadded as the copies fill them (a wave instruction fills 64 consecutive 16-byte
+// chunks), with an XOR swizzle of the chunk index that keeps the operand reads
+// conflict-free under the LDS bank model:
+//   k-contiguous ([ROWS][32]: 4 chunks per row): chunk c of row r at c ^ ((r >> 2) & 3).
+//     A row fragment read (32 rows, one chunk per half-wave) then covers 16 distinct
+//     16-byte slots in each 16-lane pass.
+//   k-strided ([32][ROWS]: ROWS / 8 chunks per k row, rows a multiple of 256 bytes):
+//     chunk c of k row r at c ^ (4 (r & 3)). A transposing read covers 4 consecutive
+//     k rows x 4 chunks per half-wave, which the XOR spreads over the four 64-byte
+//     quarters of the banks.
+constexpr int kGK = 32;  // contraction per stage
+
+// This lane's share of the copies of one operand tile (ROWS / 16 instructions, wave w
+// issues w, w + 4, ...).
+template <bool KS, int ROWS>
+struct GFill {
+  static constexpr int NI = ROWS / 16, PER = NI / 4, CPR = ROWS / 8;
+  uint32_t off[PER];  // byte offsets from the stage origin of the operand
+  // r0: first row (column for KS) of the tile; rlim: number of rows (columns) in the operand.
+  __device__ __forceinline__ void init(int wave, int l, int ld, int r0, int rlim) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int p = (wave + 4 * i) * 64 + l;
+      if (!KS) {
+        const int row = p >> 2, c = (p & 3) ^ ((row >> 2) & 3);
+        off[i] = 2u * (uint32_t)(min(r0 + row, rlim - 1) * ld + c * 8);  // rows past the end read the last
+      } else {
+        const int kr = p / CPR, c = (p % CPR) ^ (4 * (kr & 3));
+        off[i] = 2u * (uint32_t)(kr * ld + min(r0 + c * 8, rlim - 8));  // columns past the end likewise
+      }
+    }
+  }
+  __device__ __forceinline__ void fill(const bf16* stage_origin, bf16* tile, int wave) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) g2lds16_so(stage_origin, off[i], tile + (wave + 4 * i) * 512);
+  }
+};
+
+// Operand fragments of one wave's four 32-row blocks (rows 128 wsel .. +127 of the
+// tile), contraction step ks (16 wide) of the stage.
+template <bool KS, int ROWS>
+struct GRead {
+  int off[4];  // element offsets: k-contiguous uses [0..1] (per ks), k-strided [0..3] (per block)
+  __device__ __forceinline__ void init(int l, int wsel) {
+    const int g = l >> 5;
+    if (!KS) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) off[ks] = (l & 31) * kGK + ((2 * ks + g) ^ ((l >> 2) & 3)) * 8;
+    } else {
+      // transposing read of k rows ra + s/4 (ra = 16 ks + 8 g; second half ra + 4) and
+      // columns 32 b + 16 ((l >> 4) & 1) + 4 (s & 3) .. +3, s = l % 16, b = 4 wsel + j
+      const int s = l & 15, j4 = s >> 2, lc = 2 * ((l >> 4) & 1) + ((s & 3) >> 1);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        off[j] = j4 * ROWS + 8 * g * ROWS + (4 * (4 * wsel + (j ^ j4)) + lc) * 8 + 4 * (s & 1);
+    }
+  }
+  __device__ __forceinline__ bf16x8 get(const bf16* tile, int wsel, int ks, int j) const {
+    if (!KS) return *reinterpret_cast<const bf16x8*>(tile + (128 * wsel + 32 * j) * kGK + off[ks]);
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    const bf16* p = tile + off[j] + 16 * ks * ROWS;
+    const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+    const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * ROWS));
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
+};
+
+// C (+ blockIdx.z * split_stride) [M][N] = A[M][k range] B[k range][N], bf16 operands,
+// fp32 accumulation. SPLIT as in gemm_kernel (1: A + X2, 2: B + X2; hi before lo per
+// k-step). The k range of a split is a multiple of 32; M, N multiples of 8.
+template <int BM, int BN, bool A_KS, bool B_KS, int SPLIT, typename TO>
+__global__ __launch_bounds__(256, 1) void gemm_big_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ B, const bf16* __restrict__ X2, TO* __restrict__ C,
+    int M, int N, int K, int lda, int ldb, int ldc, int k_chunk, long long split_stride) {
+  static_assert(BM * BN == 4 * 128 * 128 && BM % 128 == 0 && BN % 128 == 0, "four 128 x 128 waves");
+  constexpr int WM = BM / 128;                     // waves along m
+  constexpr int NT = SPLIT ? 3 : 2;                // operand tiles per stage: A, B (, X2)
+  constexpr int NSLOT = SPLIT ? 3 : 4;             // ring depth (LDS: 144 or 128 KB)
+  constexpr bool X_KS = SPLIT == 1 ? A_KS : B_KS;
+  constexpr int XR = SPLIT == 1 ? BM : BN;         // rows of the X2 tile
+  constexpr int TA = BM * kGK, TB = BN * kGK, TX = SPLIT ? XR * kGK : 0;
+  constexpr int STAGE = TA + TB + TX;              // elements per stage
+  __shared__ __attribute__((aligned(16))) bf16 sm[NSLOT * STAGE];
+
+  const int n_tiles = (N + BN - 1) / BN, m_tiles = (M + BM - 1) / BM;
+  const int lin = xcd_remap(blockIdx.x, n_tiles * m_tiles);
+  const int tn = lin % n_tiles, tm = lin / n_tiles;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kb = blockIdx.z * k_chunk;
+  const int nst = (min(K, kb + k_chunk) - kb) / kGK;  // stages
+
+  const int l = threadIdx.x & 63, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;
+  const int wm = wave % WM, wn = wave / WM;
+
+  GFill<A_KS, BM> fa;
+  GFill<B_KS, BN> fb;
+  GFill<X_KS, XR> fx;
+  fa.init(wave, l, lda, m0, M);
+  fb.init(wave, l, ldb, n0, N);
+  if (SPLIT) fx.init(wave, l, SPLIT == 1 ? lda : ldb, SPLIT == 1 ? m0 : n0, SPLIT == 1 ? M : N);
+  auto fill = [&](int slot, int k) {
+    bf16* st = sm + slot * STAGE;
+    fa.fill(A_KS ? A + (size_t)k * lda : A + k, st, wave);
+    fb.fill(B_KS ? B + (size_t)k * ldb : B + k, st + TA, wave);
+    if (SPLIT == 1) fx.fill(A_KS ? X2 + (size_t)k * lda : X2 + k, st + TA + TB, wave);
+    if (SPLIT == 2) fx.fill(B_KS ? X2 + (size_t)k * ldb : X2 + k, st + TA + TB, wave);
+  };
+  constexpr int F = GFill<A_KS, BM>::PER + GFill<B_KS, BN>::PER + (SPLIT ? GFill<X_KS, XR>::PER : 0);
+  // wait until the copies of a stage have landed while `ahead` later stages may still
+  // be in flight (copies complete in issue order)
+  auto wait_stage = [](int ahead) {
+    if (ahead >= 3) wait_vmem_le<3 * F>();
+    else if (ahead == 2) wait_vmem_le<2 * F>();
+    else if (ahead == 1) wait_vmem_le<F>();
+    else wait_vmem();
+  };
+  static_assert(NSLOT <= 4 && 3 * F < 64, "vmcnt range");
+
+  GRead<A_KS, BM> ra;
+  GRead<B_KS, BN> rb;
+  GRead<X_KS, XR> rx;
+  ra.init(l, wm);
+  rb.init(l, wn);
+  const int xsel = SPLIT == 1 ? wm : wn;
+  if (SPLIT) rx.init(l, xsel);
+
+  f32x16 acc[4][4];  // [n block][m block]: C^T blocks, lane <-> m, 4 consecutive n per lane
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[j][i] = f32x16{};
+
+  bf16x8 fA[2][4], fB[2][4], fX[2][4];  // operands of contraction steps 0 and 1 of a stage
+  auto read = [&](int slot, int ks) {
+    const bf16* st = sm + slot * STAGE;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      fA[ks][j] = ra.get(st, wm, ks, j);
+      fB[ks][j] = rb.get(st + TA, wn, ks, j);
+      if (SPLIT) fX[ks][j] = rx.get(st + TA + TB, xsel, ks, j);
+    }
+  };
+  auto mmas = [&](int ks, int j0, int j1) {  // n blocks [j0, j1) of step ks
+#pragma unroll
+    for (int j = j0; j < j1; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        mma(acc[j][i], fB[ks][j], fA[ks][i]);
+        if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
+        if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
+      }
+  };
+
+  const int npre = min(NSLOT, nst);
+  for (int t = 0; t < npre; ++t) fill(t, kb + t * kGK);
+  wait_stage(npre - 1);  // stage 0 has landed
+  lds_barrier();
+  read(0, 0);
+  // (the last stage is peeled: every trip of the loop then ends with the next stage's
+  // first operands in flight, and the compiler's LDS waits stay exact)
+  // Instruction order within a stage (the scheduler would otherwise bunch the LDS
+  // reads and the waits on them): step-1 reads interleaved with the step-0 MFMAs, in
+  // four groups; then half of the step-1 MFMAs; barrier and copies; the next stage's
+  // step-0 reads interleaved with the other half.
+  constexpr int RPS = (A_KS ? 8 : 4) + (B_KS ? 8 : 4) + (SPLIT ? (X_KS ? 8 : 4) : 0);  // LDS reads per step
+  constexpr int MPJ = SPLIT ? 8 : 4;  // MFMAs per n block and step
+  constexpr int DS_READ = 0x100, MFMA = 0x008;
+  for (int t = 0; t < nst - 1; ++t) {
+    const int slot = t % NSLOT;
+    read(slot, 1);
+    mmas(0, 0, 4);
+    mmas(1, 0, 2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 4, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, MPJ, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(MFMA, 2 * MPJ, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_stage(min(NSLOT - 2, nst - 2 - t));  // this wave's copies of stage t + 1 have landed
+    lds_barrier();  // ... everyone's; and every read of stage t is done
+    if (t + NSLOT < nst) fill(slot, kb + (t + NSLOT) * kGK);
+    __builtin_amdgcn_sched_barrier(0);
+    read((t + 1) % NSLOT, 0);
+    mmas(1, 2, 4);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 2, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, MPJ, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  read((nst - 1) % NSLOT, 1);
+  mmas(0, 0, 4);
+  mmas(1, 0, 4);
+
+  TO* Cz = C + blockIdx.z * split_stride;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + 128 * wm + 32 * i + (l & 31);
+      if (m >= M) continue;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int n = n0 + 128 * wn + 32 * j + rr * 8 + g * 4;
+        if (n < N)
+          store4<TO>(Cz + (size_t)m * ldc + n, acc[j][i][4 * rr], acc[j][i][4 * rr + 1], acc[j][i][4 * rr + 2],
+                     acc[j][i][4 * rr + 3]);
+      }
+    }
+}
+
+// The large-tile kernel applies to bf16 operands whose contraction range splits into
+// multiples of 32, with M and N multiples of 8, and whose byte offsets within an
+// operand fit the 32-bit offsets of the copies.
+bool gemm_big_ok(int M, int N, int K, int k_chunk, size_t a_elems, size_t b_elems) {
+  return K % kGK == 0 && k_chunk % kGK == 0 && M % 8 == 0 && N % 8 == 0 && M >= 8 && N >= 8 &&
+         2 * a_elems < (1ull << 32) && 2 * b_elems < (1ull << 32);
+}
+
 // dst[i] = sum_{s < nsplit} src[s * stride + i], in ascending s (float4 granularity).
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ src, float* __restrict__ dst,
                                                            long long n4, int nsplit, long long stride) {
@@ -218,6 +456,13 @@ inline int grid_tiles(int M, int N, int BM, int BN) { return ((M + BM - 1) / BM)
 template <typename T>
 hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st) {
   using G = GemmCfg<T>;
+  if constexpr (sizeof(T) == 2) {
+    if (gemm_big_ok(M, N, K, K, (size_t)M * K, (size_t)K * N)) {
+      gemm_big_kernel<256, 256, false, true, 0, bf16><<<grid_tiles(M, N, 256, 256), 256, 0, st>>>(
+          c, w, nullptr, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N, /*k_chunk=*/K, 0);
+      return hipGetLastError();
+    }
+  }
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, 1);
   gemm_kernel<T, T, false, true, G::BM, G::BN, G::BK, 0><<<grid, kThreads, 0, st>>>(
       c, w, nullptr, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N, /*k_chunk=*/K, 0);
@@ -226,6 +471,8 @@ hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K
 
 namespace {
 constexpr int kMinGemmBlocks = 512;  // workgroups wanted per GEMM launch (256 CUs)
+// dc's output has d_c columns: a side of more than 256 takes 128 x 512 tiles (dKV read once)
+inline int dc_bm(int d_c) { return d_c > 256 ? 128 : 256; }
 }  // namespace
 
 int dw_split_tokens(int tokens) {
@@ -238,9 +485,13 @@ size_t dw_split_count(int tokens) {
   return (size_t)((tokens + s - 1) / s);
 }
 int dc_split_count(int tokens, int d_c, int K) {
-  const int tiles = grid_tiles(tokens, d_c, GemmCfg<bf16>::BM, GemmCfg<bf16>::BN);
+  const bool big = gemm_big_ok(tokens, d_c, K, kGK, (size_t)tokens * K, (size_t)d_c * K);
+  const int tiles = big ? grid_tiles(tokens, d_c, dc_bm(d_c), 65536 / dc_bm(d_c))
+                        : grid_tiles(tokens, d_c, GemmCfg<bf16>::BM, GemmCfg<bf16>::BN);
   const int max_split = K / 256;  // at least one head (256 contraction indices) per split
-  int n = (kMinGemmBlocks + tiles - 1) / tiles;
+  // large tiles: one workgroup per CU (256) is enough; small tiles want two or more
+  const int want = big ? 256 : kMinGemmBlocks;
+  int n = (want + tiles - 1) / tiles;
   return n < 1 ? 1 : (n > max_split ? max_split : n);
 }
 size_t gemm_partial_elems(int tokens, int d_c, int K) {
@@ -261,7 +512,19 @@ hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, float
   const int nz = (K + k_chunk - 1) / k_chunk;
   float* target = nz == 1 ? dc : partial;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, nz);
-  if (dkv_lo)
+  if constexpr (sizeof(T) == 2) {
+    if (dkv_lo && gemm_big_ok(M, N, K, k_chunk, (size_t)M * K, (size_t)N * K)) {
+      if (dc_bm(N) == 128)
+        gemm_big_kernel<128, 512, false, false, 1, float><<<dim3(grid_tiles(M, N, 128, 512), 1, nz), 256, 0, st>>>(
+            dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
+      else
+        gemm_big_kernel<256, 256, false, false, 1, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 256, 0, st>>>(
+            dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
+      grid.x = 0;  // done
+    }
+  }
+  if (grid.x == 0) {
+  } else if (dkv_lo)
     gemm_kernel<T, float, false, false, G::BM, G::BN, G::BK, 1><<<grid, kThreads, 0, st>>>(
         dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
   else
@@ -283,7 +546,19 @@ hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float
   const int nsplit = (int)dw_split_count(K);
   float* target = nsplit == 1 ? dw : partial;
   dim3 grid(grid_tiles(M, N, G::BM, G::BN), 1, nsplit);
-  if (dkv_lo)
+  if constexpr (sizeof(T) == 2) {
+    if (dkv_lo && gemm_big_ok(M, N, K, split, (size_t)K * M, (size_t)K * N)) {
+      if (M > 256)
+        gemm_big_kernel<512, 128, true, true, 2, float><<<dim3(grid_tiles(M, N, 512, 128), 1, nsplit), 256, 0, st>>>(
+            c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
+      else
+        gemm_big_kernel<256, 256, true, true, 2, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nsplit), 256, 0, st>>>(
+            c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
+      grid.x = 0;  // done
+    }
+  }
+  if (grid.x == 0) {
+  } else if (dkv_lo)
     gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 2><<<grid, kThreads, 0, st>>>(
         c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
   else
