@@ -59,8 +59,11 @@ def test_tiny_fp32(S, B, causal):
     check_full(LI.WORKLOADS["tiny_fp32"].replace(seq_len=S, batch=B, causal=causal))
 
 
+# (288, 3, 1): the large-tile GEMMs with partial tiles (tokens 288 = 256 + 32; dc split
+# over heads; dW over 288 tokens); (264, 2, 2): likewise with batch 2, non-causal.
 @pytest.mark.parametrize("S,H,B,causal", [(2048, 16, 1, True), (1, 1, 1, True), (7, 3, 2, True),
-                                          (257, 3, 2, True), (300, 2, 1, False)])
+                                          (257, 3, 2, True), (300, 2, 1, False), (288, 3, 1, True),
+                                          (264, 2, 2, False)])
 def test_v3_bf16(S, H, B, causal):
     check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal))
 

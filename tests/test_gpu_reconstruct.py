@@ -25,7 +25,8 @@ def test_fp32(name, S):
     assert err(got, ref) < TOL["fp32"]
 
 
-@pytest.mark.parametrize("S,H", [(4096, 16), (1, 16), (333, 3), (129, 1)])
+# 520 and 1000 tokens: the large-tile kernel with a partial last row of tiles
+@pytest.mark.parametrize("S,H", [(4096, 16), (1, 16), (333, 3), (129, 1), (520, 3), (1000, 16)])
 def test_bf16(S, H):
     w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=S, n_heads=H)
     got, ref, _, _ = run(w)
