@@ -669,7 +669,11 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t st) {
   using Tl = FwdTiles<T, DN, DR, DV>;
-  constexpr int BR = 32 * Tl::WPH;
+  // bf16: 8 waves, so 256 queries of the workgroup share each rebuilt K/V tile (the
+  // rebuild costs d_c * d_kvh / Br times the attention flops; 4 waves: 13.3 ms at
+  // S = 16384, 8 waves: 5.7 ms)
+  constexpr int FW = sizeof(T) == 2 ? 8 : Tl::WPH;
+  constexpr int BR = 32 * FW;
   const int N = a.H * (DN + DV);
   const long long nw = (long long)a.d_c * N;
   transpose_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
@@ -679,7 +683,7 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
   P.scale_log2 = a.scale * 1.4426950408889634f;
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * a.H, a.B, 1);
-  attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, kFusedMaxDc><<<grid, 64 * Tl::WPH, 0, st>>>(P);
+  attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, FW, kFusedMaxDc><<<grid, 64 * FW, 0, st>>>(P);
   return hipGetLastError();
 }
 
