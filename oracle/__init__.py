@@ -10,10 +10,15 @@ Modules:
   * ``absorbed`` — the algebraically equivalent absorbed form (B2), used only
                    as a pin of ``laga``; it materialises n_h*d_c intermediates,
                    which is fine on the CPU and never happens on the GPU.
+  * ``producers`` — the per-token producers around the latent all-gather: the
+                   latent RMS normalisation (Alg. 1 step 1) and the decoupled
+                   rotary embedding of k_pe / q_rope, with their backward.
 
-Parity status: every function here is pinned by tests/test_oracle.py
+Parity status: every function of ``laga`` is pinned by tests/test_oracle.py
 (brute force, absorbed form, finite differences, closed forms, invariants,
-causal prefix, torch SDPA). The paper prints no worked numeric example of the
+causal prefix, torch SDPA), every one of ``producers`` by
+tests/test_producers_oracle.py (hand-computed rotations, closed forms, rotation
+algebra, finite differences). The paper prints no worked numeric example of the
 attention outputs, so no pin compares against values printed in the paper.
 """
 from .laga import (reconstruct_kv, attn_fwd, attn_bwd, attn_fwd_rows,
