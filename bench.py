@@ -224,6 +224,8 @@ def gpu_bench(w, steps, warmup, fused_compare):
            "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
     assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
 
+    res["prologue"] = prologue_bench(w, p, steps, warmup)
+
     if fused_compare:
         pf = L.Problem(**{**p.__dict__, "kv_mode": L.KV_FUSED})
         ws_ff = torch.empty(max(1, L.laga_workspace_bytes(pf, L.OP_FWD)), dtype=torch.uint8, device=dev)
@@ -242,6 +244,59 @@ def gpu_bench(w, steps, warmup, fused_compare):
             res["fused_fwd_ms"] = None
             res["fused_error"] = str(e)
     return res
+
+
+def prologue_bench(w, p, steps, warmup):
+    """The producers around the latent all-gather (latent RMS normalisation with a weight,
+    RoPE of k_pe and of every head's q_rope band; and their backward) at the workload's
+    shape, timed apart from the step. HBM-bound: reported against 8 TB/s with the
+    algorithmic bytes (every input read once, every output written once)."""
+    import torch
+    import laga_inputs as LI
+    import paper_2607_17644_amd as L
+
+    x = LI.make_prologue_inputs(w)
+    dev = torch.device("cuda:0")
+    d = {k: torch.from_numpy(v).to(torch.float32 if k in ("dc_kv", "dk_pe") else torch.bfloat16).to(dev)
+         for k, v in x.items()}
+    sh = p.shapes()
+    c_kv = torch.empty(sh["c_kv"], dtype=torch.bfloat16, device=dev)
+    k_pe = torch.empty(sh["k_pe"], dtype=torch.bfloat16, device=dev)
+    rstd = torch.empty((w.batch, w.seq_len), dtype=torch.float32, device=dev)
+    d_lat = torch.empty(sh["dc_kv"], dtype=torch.float32, device=dev)
+    d_kpe = torch.empty(sh["dk_pe"], dtype=torch.float32, device=dev)
+    d_gamma = torch.empty((w.d_c,), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, L.laga_workspace_bytes(p, L.OP_PROLOGUE_BWD)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fwd():
+        L.laga_prologue_fwd(p, d["latent_raw"], d["kpe_raw"], q=d["q"], gamma=d["gamma"], c_kv=c_kv, k_pe=k_pe,
+                            rstd=rstd, stream=stream)
+
+    def bwd():
+        L.laga_prologue_bwd(p, d["latent_raw"], rstd, d["dc_kv"], d["dk_pe"], dq=d["dq"], gamma=d["gamma"],
+                            d_latent_raw=d_lat, d_kpe_raw=d_kpe, d_gamma=d_gamma, workspace=ws, stream=stream)
+
+    tok, H, dc, dr = w.batch * w.seq_len, w.n_heads, w.d_c, w.d_rope
+    nbytes = {"fwd": tok * (2 * dc + 2 * dr + 2 * H * dr) * 2 + tok * 4 + 2 * dc,
+              "bwd": tok * (2 * dc + 4 + 4 * dc + 4 * dr + 2 * H * dr) + tok * (4 * dc + 4 * dr + 2 * H * dr)
+              + 2 * dc + 4 * dc}
+    out = {}
+    n = max(steps, 20)
+    for name, fn in (("fwd", fwd), ("bwd", bwd)):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        gbs = nbytes[name] / (ms * 1e-3) / 1e9
+        out[name] = {"ms": round(ms, 5), "algorithmic_bytes": nbytes[name], "GB/s": round(gbs, 1),
+                     "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
 
 
 def cpu_baseline(w, heads):
@@ -325,6 +380,7 @@ def main():
         "ms_min_max_step": [round(g["ms_min_step"], 4), round(g["ms_max_step"], 4)],
         "roofline": roofline,
         "algorithmic_tflops_by_kernel": other,
+        "prologue_outside_step": g.get("prologue"),
         "cpu_baseline": cpu,
     }
     if a.fused_compare:

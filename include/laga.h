@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define LAGA_ABI_VERSION 1
+#define LAGA_ABI_VERSION 2
 
 typedef enum {
   LAGA_OK = 0,
@@ -90,7 +90,7 @@ typedef enum { LAGA_DTYPE_BF16 = 0, LAGA_DTYPE_FP32 = 1 } laga_dtype_t;
  *        tensor is ever written to HBM by the forward. */
 typedef enum { LAGA_KV_MATERIALIZED = 0, LAGA_KV_FUSED = 1 } laga_kv_mode_t;
 
-typedef enum { LAGA_OP_FWD = 0, LAGA_OP_BWD = 1 } laga_op_t;
+typedef enum { LAGA_OP_FWD = 0, LAGA_OP_BWD = 1, LAGA_OP_PROLOGUE_BWD = 2 } laga_op_t;
 
 typedef struct {
   int64_t batch;       /* B */
@@ -166,6 +166,56 @@ LAGA_API laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p,
                                            void* dq, float* dc_kv, float* dk_pe,
                                            float* dw_kv_b, void* workspace,
                                            size_t workspace_bytes, void* stream);
+
+/* ---- Producers around the latent all-gather ---------------------------------
+ * The per-token steps that make this block's inputs and consume its gradients
+ * (Alg. 1 step 1's latent normalisation; the decoupled RoPE of Section 2.1,
+ * property P2, and Section 5.3). Token t of the sequence axis sits at position
+ * p = position_offset + t (0 for the gathered sequence; a rank's chunk of S/P
+ * tokens starts at r*S/P). R(p) rotates each pair (2i, 2i+1) of a d_rope-wide
+ * band counter-clockwise by p * rope_base^(-2i/d_rope):
+ * (x0, x1) -> (x0 cos - x1 sin, x0 sin + x1 cos). The problem must be valid as
+ * for the attention calls; its softmax_scale, causal and kv_mode are not used. */
+typedef struct {
+  float eps;               /* added to the mean square, >= 0 (e.g. 1e-6) */
+  float rope_base;         /* rotary base, > 1 (e.g. 10000) */
+  int64_t position_offset; /* position of token 0, 0 <= offset, offset + S < 2^53 */
+} laga_prologue_t;
+
+/* Forward, per token (b, t):
+ *   rstd[b,t]  = 1 / sqrt(mean_j latent_raw[b,t,j]^2 + eps)               fp32 [B,S]
+ *   c_kv[b,t,j] = latent_raw[b,t,j] * rstd[b,t] * gamma[j]  (gamma NULL: 1) [B,S,d_c]
+ *   k_pe[b,t,:] = R(p) kpe_raw[b,t,:]                                      [B,S,d_rope]
+ *   q[b,t,h,d_nope:] = R(p) q[b,t,h,d_nope:] for every head, IN PLACE; the
+ *                      q_nope columns are left untouched; q may be NULL.
+ * latent_raw [B,S,d_c], gamma [d_c], kpe_raw [B,S,d_rope] and q [B,S,H,d_nope+
+ * d_rope] are in the element dtype, as are c_kv and k_pe. Statistics in fp32.
+ * No workspace. Errors: LAGA_ERR_NULL (problem, cfg or a required pointer),
+ * LAGA_ERR_SHAPE (eps < 0, rope_base <= 1, offset out of range, or the problem),
+ * LAGA_ERR_ALIGN, LAGA_ERR_UNSUPPORTED (dims as for the attention calls). */
+LAGA_API laga_status_t laga_prologue_fwd(const laga_problem_t* p, const laga_prologue_t* cfg,
+                                         const void* latent_raw, const void* gamma,
+                                         const void* kpe_raw, void* q, void* c_kv,
+                                         void* k_pe, float* rstd, void* stream);
+
+/* Backward of laga_prologue_fwd, given the complete fp32 gradients dc_kv [B,S,d_c]
+ * and dk_pe [B,S,d_rope] (on one rank with every head: laga_attn_bwd's; across
+ * ranks: after the reduce-scatter of Section 5.2) and dq:
+ *   d_latent_raw = rstd * (g - y * mean_j(g y)),  y = rstd * latent_raw,
+ *                  g = gamma * dc_kv (gamma NULL: dc_kv)                 fp32 [B,S,d_c]
+ *   d_gamma[j]   = sum over (b, t) of dc_kv[b,t,j] * y[b,t,j], in a fixed order
+ *                  (bitwise repeatable)           fp32 [d_c]; required iff gamma given
+ *   d_kpe_raw    = R(p)^T dk_pe                                        fp32 [B,S,d_rope]
+ *   dq[b,t,h,d_nope:] = R(p)^T dq[b,t,h,d_nope:], IN PLACE (element dtype); may be NULL.
+ * rstd is the forward's. With gamma the workspace must hold
+ * laga_workspace_bytes(p, LAGA_OP_PROLOGUE_BWD) bytes (partial sums of d_gamma);
+ * without, it may be NULL. Errors as for the forward, plus LAGA_ERR_WORKSPACE. */
+LAGA_API laga_status_t laga_prologue_bwd(const laga_problem_t* p, const laga_prologue_t* cfg,
+                                         const void* latent_raw, const void* gamma,
+                                         const float* rstd, const float* dc_kv,
+                                         const float* dk_pe, void* dq, float* d_latent_raw,
+                                         float* d_kpe_raw, float* d_gamma, void* workspace,
+                                         size_t workspace_bytes, void* stream);
 
 /* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
  * is invalid (check with the entry point itself for the error code). For the

@@ -7,10 +7,13 @@ sharing method code.
 What it does, in order:
   * draws every tensor from one numpy PCG64 stream (seeded) in a fixed order:
     c_raw, kpe_raw, q_nope, q_rope, W_kv_b, dO;
-  * applies the two upstream producers that run *before* the latent all-gather
-    (Alg. 1 step 1): an RMS normalisation of the latent (no weight, eps 1e-6)
-    and the decoupled rotary embedding of the rope bands (interleaved pairs
-    (2i, 2i+1) rotated by pos * 10000^(-2i/d_rope), positions 0..S-1);
+  * shapes the attention block's inputs as the workload recipe states: an RMS
+    normalisation of the latent (no weight, eps 1e-6) and a rotation of the rope
+    bands (interleaved pairs (2i, 2i+1) by pos * 10000^(-2i/d_rope), positions
+    0..S-1). These two helpers only give the synthetic inputs their distribution;
+    the library's producer entry points (laga_prologue_fwd / _bwd) and their
+    oracle are separate implementations, tested on the raw draws of
+    ``make_prologue_inputs``, never against these helpers;
   * rounds each tensor to the element dtype (round-to-nearest-even for bf16),
     so that the oracle (which upcasts to fp64) and the GPU see the same values.
 
@@ -26,7 +29,8 @@ import math
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "make_inputs", "round_bf16", "rope", "rms_normalize"]
+__all__ = ["Workload", "WORKLOADS", "make_inputs", "make_prologue_inputs", "round_bf16", "rope",
+           "rms_normalize"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -166,3 +170,34 @@ def make_inputs(w: Workload, with_dout: bool = True) -> dict:
     if with_dout:
         out["dout"] = round_to(dout, w.dtype)
     return out
+
+
+def make_prologue_inputs(w: Workload, seed_offset: int = 1) -> dict:
+    """Raw (pre-normalisation, pre-rotation) inputs of the producers around the latent
+    all-gather, and upstream gradients for their backward, with the shapes of ``w``.
+
+    Keys: latent_raw [B,S,d_c] (each token's row at its own scale, log-uniform over
+    about two decades, as a projection output would be), gamma [d_c] (U(0.5, 1.5)),
+    kpe_raw [B,S,d_rope], q [B,S,H,d_nope+d_rope] (unrotated), all in w.dtype;
+    dc_kv [B,S,d_c], dk_pe [B,S,d_rope] (float32 gradients) and dq
+    [B,S,H,d_nope+d_rope] (in w.dtype). Drawn from its own stream (seed + seed_offset).
+    """
+    rng = np.random.Generator(np.random.PCG64(w.seed + seed_offset))
+    B, S, H = w.batch, w.seq_len, w.n_heads
+    scale = np.exp(rng.uniform(np.log(0.1), np.log(10.0), (B, S, 1)))
+    latent = rng.standard_normal((B, S, w.d_c)) * scale
+    gamma = rng.uniform(0.5, 1.5, w.d_c)
+    kpe = rng.standard_normal((B, S, w.d_rope))
+    q = rng.standard_normal((B, S, H, w.d_qk))
+    dc = rng.standard_normal((B, S, w.d_c))
+    dk = rng.standard_normal((B, S, w.d_rope))
+    dq = rng.standard_normal((B, S, H, w.d_qk))
+    return {
+        "latent_raw": round_to(latent, w.dtype),
+        "gamma": round_to(gamma, w.dtype),
+        "kpe_raw": round_to(kpe, w.dtype),
+        "q": round_to(q, w.dtype),
+        "dc_kv": dc.astype(np.float32),
+        "dk_pe": dk.astype(np.float32),
+        "dq": round_to(dq, w.dtype),
+    }

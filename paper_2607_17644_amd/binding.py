@@ -19,7 +19,7 @@ lib_path = os.path.join(_PKG, "liblaga.so")
 
 DTYPE_BF16, DTYPE_FP32 = 0, 1
 KV_MATERIALIZED, KV_FUSED = 0, 1
-OP_FWD, OP_BWD = 0, 1
+OP_FWD, OP_BWD, OP_PROLOGUE_BWD = 0, 1, 2
 BWD_PREPARE, BWD_DKDV, BWD_DQ, BWD_FINISH = 0, 1, 2, 3
 
 _STATUS = {0: "LAGA_OK", 1: "LAGA_ERR_NULL", 2: "LAGA_ERR_SHAPE", 3: "LAGA_ERR_UNSUPPORTED",
@@ -38,6 +38,10 @@ class _CProblem(ctypes.Structure):
                 ("d_v", ctypes.c_int64), ("softmax_scale", ctypes.c_float), ("causal", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("kv_mode", ctypes.c_int32), ("deterministic", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
+
+
+class _CPrologue(ctypes.Structure):
+    _fields_ = [("eps", ctypes.c_float), ("rope_base", ctypes.c_float), ("position_offset", ctypes.c_int64)]
 
 
 @dataclasses.dataclass
@@ -97,6 +101,11 @@ def _load():
     L.laga_attn_bwd_stage.restype = ctypes.c_int
     L.laga_attn_bwd_stage.argtypes = [ctypes.c_int, P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       ctypes.c_size_t, vp]
+    Q = ctypes.POINTER(_CPrologue)
+    L.laga_prologue_fwd.restype = ctypes.c_int
+    L.laga_prologue_fwd.argtypes = [P, Q, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.laga_prologue_bwd.restype = ctypes.c_int
+    L.laga_prologue_bwd.argtypes = [P, Q, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     return L
 
 
@@ -227,3 +236,56 @@ def laga_attn_bwd_stage(stage: int, p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, 
     _check(_lib.laga_attn_bwd_stage(stage, *_bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq,
                                                        dc_kv, dk_pe, dw_kv_b, workspace), _stream(stream)),
            "laga_attn_bwd_stage")
+
+
+def laga_prologue_fwd(p: Problem, latent_raw, kpe_raw, q=None, gamma=None, eps=1e-6, rope_base=10000.0,
+                      position_offset=0, c_kv=None, k_pe=None, rstd=None, stream=None):
+    """Latent normalisation and decoupled RoPE before the all-gather; returns (c_kv, k_pe,
+    rstd). The q_rope columns of q (if given) are rotated in place."""
+    sh, dt = p.shapes(), p.torch_dtype
+    dev = latent_raw.device
+    if c_kv is None:
+        c_kv = _new(p, "c_kv", dt, dev)
+    if k_pe is None:
+        k_pe = _new(p, "k_pe", dt, dev)
+    if rstd is None:
+        rstd = torch.empty((p.batch, p.seq_len), dtype=torch.float32, device=dev)
+    cfg = _CPrologue(eps, rope_base, position_offset)
+    _check(_lib.laga_prologue_fwd(
+        ctypes.byref(p.c()), ctypes.byref(cfg), _ptr(latent_raw, "latent_raw", sh["c_kv"], dt),
+        _ptr(gamma, "gamma", (p.d_c,), dt, required=False), _ptr(kpe_raw, "kpe_raw", sh["k_pe"], dt),
+        _ptr(q, "q", sh["q"], dt, required=False), _ptr(c_kv, "c_kv", sh["c_kv"], dt),
+        _ptr(k_pe, "k_pe", sh["k_pe"], dt), _ptr(rstd, "rstd", (p.batch, p.seq_len), torch.float32),
+        _stream(stream)), "laga_prologue_fwd")
+    return c_kv, k_pe, rstd
+
+
+def laga_prologue_bwd(p: Problem, latent_raw, rstd, dc_kv, dk_pe, dq=None, gamma=None, eps=1e-6,
+                      rope_base=10000.0, position_offset=0, d_latent_raw=None, d_kpe_raw=None, d_gamma=None,
+                      workspace=None, stream=None):
+    """Backward of laga_prologue_fwd; returns (d_latent_raw, d_kpe_raw, d_gamma) in fp32
+    (d_gamma None without gamma). The q_rope columns of dq (if given) are rotated back in place."""
+    sh, dt = p.shapes(), p.torch_dtype
+    dev = latent_raw.device
+    if d_latent_raw is None:
+        d_latent_raw = _new(p, "dc_kv", torch.float32, dev)
+    if d_kpe_raw is None:
+        d_kpe_raw = _new(p, "dk_pe", torch.float32, dev)
+    if gamma is not None and d_gamma is None:
+        d_gamma = torch.empty((p.d_c,), dtype=torch.float32, device=dev)
+    nbytes = 0
+    if gamma is not None:
+        workspace = _workspace(p, OP_PROLOGUE_BWD, workspace, dev)
+        nbytes = workspace.numel() * workspace.element_size()
+    cfg = _CPrologue(eps, rope_base, position_offset)
+    _check(_lib.laga_prologue_bwd(
+        ctypes.byref(p.c()), ctypes.byref(cfg), _ptr(latent_raw, "latent_raw", sh["c_kv"], dt),
+        _ptr(gamma, "gamma", (p.d_c,), dt, required=False),
+        _ptr(rstd, "rstd", (p.batch, p.seq_len), torch.float32),
+        _ptr(dc_kv, "dc_kv", sh["dc_kv"], torch.float32), _ptr(dk_pe, "dk_pe", sh["dk_pe"], torch.float32),
+        _ptr(dq, "dq", sh["dq"], dt, required=False),
+        _ptr(d_latent_raw, "d_latent_raw", sh["dc_kv"], torch.float32),
+        _ptr(d_kpe_raw, "d_kpe_raw", sh["dk_pe"], torch.float32),
+        _ptr(d_gamma, "d_gamma", (p.d_c,), torch.float32, required=gamma is not None),
+        _ptr(workspace, "workspace", required=False), nbytes, _stream(stream)), "laga_prologue_bwd")
+    return d_latent_raw, d_kpe_raw, d_gamma

@@ -85,6 +85,34 @@ size_t fwd_ws_bytes(const laga_problem_t* p, const Dims& d) {
 
 laga_status_t from_hip(hipError_t e) { return e == hipSuccess ? LAGA_OK : LAGA_ERR_DEVICE; }
 
+// Producers: d_gamma partial rows of the backward.
+size_t prologue_ws_bytes(const Dims& d) {
+  const long long tok = (long long)d.B * d.S;
+  return round_up(sizeof(float) * (size_t)(prologue_bwd_rows(tok) + prologue_sum_groups(tok)) * d.d_c);
+}
+
+laga_status_t validate_prologue(const laga_problem_t* p, const laga_prologue_t* cfg, Dims* d) {
+  if (!cfg) return LAGA_ERR_NULL;
+  laga_status_t s = validate(p, d);
+  if (s != LAGA_OK) return s;
+  if (!isfinite(cfg->eps) || cfg->eps < 0.f || !isfinite(cfg->rope_base) || !(cfg->rope_base > 1.f) ||
+      cfg->position_offset < 0 || cfg->position_offset > ((int64_t)1 << 53) - 1 - d->S)
+    return LAGA_ERR_SHAPE;
+  // the rotation kernels give each lane one 8-element chunk of a band: d_rope / 8 must divide 64
+  if (d->dr % 8 != 0 || 64 % (d->dr / 8) != 0) return LAGA_ERR_UNSUPPORTED;
+  return LAGA_OK;
+}
+
+PrologueArgs prologue_args(const laga_problem_t* p, const laga_prologue_t* cfg, const Dims& d) {
+  PrologueArgs a{};
+  a.B = d.B; a.S = d.S; a.H = d.H; a.d_c = d.d_c; a.d_nope = d.dn; a.d_rope = d.dr; a.d_qk = d.dqk();
+  a.position_offset = cfg->position_offset;
+  a.eps = cfg->eps;
+  a.log2_base = log2((double)cfg->rope_base);
+  (void)p;
+  return a;
+}
+
 template <typename T>
 laga_status_t reconstruct_t(const Dims& d, const void* c, const void* w, void* kv, hipStream_t st) {
   return from_hip(launch_reconstruct<T>((const T*)c, (const T*)w, (T*)kv, d.B * d.S, d.H * d.dkvh(), d.d_c, st));
@@ -114,7 +142,51 @@ size_t laga_workspace_bytes(const laga_problem_t* p, int op) {
   if (validate(p, &d) != LAGA_OK) return 0;
   if (op == LAGA_OP_FWD) return fwd_ws_bytes(p, d);
   if (op == LAGA_OP_BWD) return bwd_layout(p, d).total;
+  if (op == LAGA_OP_PROLOGUE_BWD) return prologue_ws_bytes(d);
   return 0;
+}
+
+laga_status_t laga_prologue_fwd(const laga_problem_t* p, const laga_prologue_t* cfg, const void* latent_raw,
+                                const void* gamma, const void* kpe_raw, void* q, void* c_kv, void* k_pe,
+                                float* rstd, void* stream) {
+  Dims d;
+  laga_status_t s = validate_prologue(p, cfg, &d);
+  if (s != LAGA_OK) return s;
+  if (!latent_raw || !kpe_raw || !c_kv || !k_pe || !rstd) return LAGA_ERR_NULL;
+  if (misaligned(latent_raw) || misaligned(kpe_raw) || misaligned(c_kv) || misaligned(k_pe) ||
+      misaligned(rstd) || (gamma && misaligned(gamma)) || (q && misaligned(q)))
+    return LAGA_ERR_ALIGN;
+  PrologueArgs a = prologue_args(p, cfg, d);
+  a.latent_raw = latent_raw; a.gamma = gamma; a.kpe_raw = kpe_raw; a.q = q; a.c_kv = c_kv; a.k_pe = k_pe;
+  a.rstd = rstd;
+  hipStream_t st = (hipStream_t)stream;
+  return from_hip(p->dtype == LAGA_DTYPE_BF16 ? launch_prologue_fwd<bf16>(a, st) : launch_prologue_fwd<float>(a, st));
+}
+
+laga_status_t laga_prologue_bwd(const laga_problem_t* p, const laga_prologue_t* cfg, const void* latent_raw,
+                                const void* gamma, const float* rstd, const float* dc_kv, const float* dk_pe,
+                                void* dq, float* d_latent_raw, float* d_kpe_raw, float* d_gamma, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  Dims d;
+  laga_status_t s = validate_prologue(p, cfg, &d);
+  if (s != LAGA_OK) return s;
+  if (!latent_raw || !rstd || !dc_kv || !dk_pe || !d_latent_raw || !d_kpe_raw || (gamma && !d_gamma))
+    return LAGA_ERR_NULL;
+  if (misaligned(latent_raw) || misaligned(rstd) || misaligned(dc_kv) || misaligned(dk_pe) ||
+      misaligned(d_latent_raw) || misaligned(d_kpe_raw) || (gamma && misaligned(gamma)) ||
+      (gamma && misaligned(d_gamma)) || (dq && misaligned(dq)))
+    return LAGA_ERR_ALIGN;
+  if (gamma) {
+    if (!workspace || workspace_bytes < prologue_ws_bytes(d)) return LAGA_ERR_WORKSPACE;
+    if (misaligned(workspace)) return LAGA_ERR_ALIGN;
+  }
+  PrologueArgs a = prologue_args(p, cfg, d);
+  a.latent_raw = latent_raw; a.gamma = gamma; a.rstd_in = rstd; a.dc_kv = dc_kv; a.dk_pe = dk_pe; a.q = dq;
+  a.d_latent = d_latent_raw; a.d_kpe = d_kpe_raw;
+  a.d_gamma = gamma ? d_gamma : nullptr;
+  a.partial = gamma ? (float*)workspace : nullptr;
+  hipStream_t st = (hipStream_t)stream;
+  return from_hip(p->dtype == LAGA_DTYPE_BF16 ? launch_prologue_bwd<bf16>(a, st) : launch_prologue_bwd<float>(a, st));
 }
 
 laga_status_t laga_reconstruct_kv(const laga_problem_t* p, const void* c_kv, const void* w_kv_b, void* kv,

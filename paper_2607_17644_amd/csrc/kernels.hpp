@@ -89,4 +89,34 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st);
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st);
 
+// Producers around the latent all-gather (latent normalisation, decoupled RoPE).
+struct PrologueArgs {
+  const void* latent_raw;  // [B,S,d_c] element dtype
+  const void* gamma;       // [d_c] element dtype, or NULL
+  const void* kpe_raw;     // forward: [B,S,d_rope]
+  void* q;                 // forward: q, backward: dq ([B,S,H,d_qk]); rope band rotated in place; or NULL
+  void* c_kv;              // forward output [B,S,d_c]
+  void* k_pe;              // forward output [B,S,d_rope]
+  float* rstd;             // forward output [B,S]
+  const float* rstd_in;    // backward input [B,S]
+  const float* dc_kv;      // backward input [B,S,d_c]
+  const float* dk_pe;      // backward input [B,S,d_rope]
+  float* d_latent;         // backward output [B,S,d_c]
+  float* d_kpe;            // backward output [B,S,d_rope]
+  float* d_gamma;          // backward output [d_c] (with gamma)
+  float* partial;          // backward workspace [prologue_bwd_rows + prologue_sum_groups][d_c] (with gamma), else NULL
+  int B, S, H, d_c, d_nope, d_rope, d_qk;
+  int64_t position_offset;
+  float eps;
+  double log2_base;
+};
+// rows of d_gamma partial sums the backward writes for `tokens` tokens
+int prologue_bwd_rows(long long tokens);
+// row groups of the fixed-order column sum of those rows
+int prologue_sum_groups(long long tokens);
+template <typename T>
+hipError_t launch_prologue_fwd(const PrologueArgs& a, hipStream_t st);
+template <typename T>
+hipError_t launch_prologue_bwd(const PrologueArgs& a, hipStream_t st);
+
 }  // namespace laga

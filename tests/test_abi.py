@@ -18,7 +18,8 @@ def declared_symbols():
 def test_header_declares_the_entry_points():
     syms = declared_symbols()
     for s in ("laga_reconstruct_kv", "laga_attn_fwd", "laga_attn_bwd", "laga_workspace_bytes",
-              "laga_status_string", "laga_abi_version"):
+              "laga_status_string", "laga_abi_version", "laga_attn_bwd_stage", "laga_prologue_fwd",
+              "laga_prologue_bwd"):
         assert s in syms
 
 
@@ -31,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     import paper_2607_17644_amd as L
-    assert L.laga_abi_version() == 1
+    assert L.laga_abi_version() == 2
     for code in range(7):
         assert L.laga_status_string(code).startswith("LAGA_")
     assert "unknown" in L.laga_status_string(99)
@@ -86,3 +87,30 @@ def test_attention_entry_points_validate_first():
     st = lib.laga_attn_bwd_stage(1, ctypes.byref(P.c()), fake, fake, fake, fake, fake, fake, fake, fake,
                                  fake, fake, fake, fake, fake, need - 1, z)
     assert st == 5
+
+
+def test_prologue_entry_points_validate_first():
+    lib, B = _raw()
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    fake = ctypes.c_void_p(0x10000)
+    z = None
+    cfg = B._CPrologue(1e-6, 10000.0, 0)
+    args = (fake, z, fake, fake, fake, fake, fake)  # latent, gamma, kpe, q, c_kv, k_pe, rstd
+    # NULL config or required pointer
+    assert lib.laga_prologue_fwd(ctypes.byref(P.c()), None, *args, z) == 1
+    assert lib.laga_prologue_fwd(ctypes.byref(P.c()), ctypes.byref(cfg), z, z, fake, fake, fake, fake, fake,
+                                 z) == 1
+    # eps < 0, rope_base <= 1, negative offset, offset + S beyond 2^53
+    for bad in (B._CPrologue(-1.0, 1e4, 0), B._CPrologue(1e-6, 1.0, 0), B._CPrologue(1e-6, 1e4, -1),
+                B._CPrologue(1e-6, float("nan"), 0), B._CPrologue(1e-6, 1e4, (1 << 53) - 10)):
+        assert lib.laga_prologue_fwd(ctypes.byref(P.c()), ctypes.byref(bad), *args, z) == 2
+    # misaligned gamma
+    assert lib.laga_prologue_fwd(ctypes.byref(P.c()), ctypes.byref(cfg), fake, ctypes.c_void_p(0x10004),
+                                 fake, fake, fake, fake, fake, z) == 4
+    # backward: gamma without d_gamma -> NULL; with gamma, workspace too small -> WORKSPACE
+    need = lib.laga_workspace_bytes(ctypes.byref(P.c()), 2)
+    assert need >= 4 * 512 and need % 256 == 0
+    bargs = [fake, fake, fake, fake, fake, fake, fake, fake]  # latent gamma rstd dc dk_pe dq d_lat d_kpe
+    assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, z, fake, need, z) == 1
+    assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, fake, fake, need - 1, z) == 5
+    assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, fake, z, need, z) == 5

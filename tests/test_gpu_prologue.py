@@ -1,0 +1,118 @@
+"""laga_prologue_fwd / laga_prologue_bwd (latent normalisation and decoupled RoPE, with
+their backward) against the oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import laga_inputs as LI
+from oracle import producers as O
+from _util import TOL, err, f64, problem_for, scaled_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def run(w, gamma=True, offset=0, eps=1e-6, base=10000.0, with_q=True):
+    import torch
+    import paper_2607_17644_amd as L
+    x = LI.make_prologue_inputs(w)
+    p = problem_for(w)
+    dev = {k: to_dev(v, w.dtype if k not in ("dc_kv", "dk_pe") else "fp32") for k, v in x.items()}
+    g = dev["gamma"] if gamma else None
+    q = dev["q"].clone() if with_q else None
+    c_kv, k_pe, rstd = L.laga_prologue_fwd(p, dev["latent_raw"], dev["kpe_raw"], q=q, gamma=g, eps=eps,
+                                           rope_base=base, position_offset=offset)
+    dq = dev["dq"].clone() if with_q else None
+    d_lat, d_kpe, d_gamma = L.laga_prologue_bwd(p, dev["latent_raw"], rstd, dev["dc_kv"], dev["dk_pe"], dq=dq,
+                                                gamma=g, eps=eps, rope_base=base, position_offset=offset)
+    torch.cuda.synchronize()
+    gam = x["gamma"] if gamma else None
+    rc, rk, rq, rr = O.prologue_forward(x["latent_raw"], x["kpe_raw"], x["q"], w.d_nope, gam, eps, base, offset)
+    rl, rkb, rqb, rg = O.prologue_backward(x["latent_raw"], x["dc_kv"], x["dk_pe"], x["dq"], w.d_nope, gam, eps,
+                                           base, offset)
+    res = {"c_kv": (f64(c_kv), rc), "k_pe": (f64(k_pe), rk), "rstd": (f64(rstd), rr),
+           "d_latent_raw": (f64(d_lat), rl), "d_kpe_raw": (f64(d_kpe), rkb)}
+    if with_q:
+        res["q"] = (f64(q), rq)
+        res["dq"] = (f64(dq), rqb)
+    if gamma:
+        res["d_gamma"] = (f64(d_gamma), rg)
+    return x, res, (q, dq, d_gamma, d_lat)
+
+
+def check(w, **kw):
+    _, res, _ = run(w, **kw)
+    tol = TOL[w.dtype]
+    msg = []
+    for name, (g, r) in res.items():
+        # d_gamma sums over every token: held to the tolerance relative to its rms
+        e = err(g, r) if name == "d_gamma" else scaled_err(g, r)
+        msg.append(f"{name} {e:.2e}")
+        assert e < tol, (name, e)
+    print(f"{w.name} S={w.seq_len} H={w.n_heads} B={w.batch} d_c={w.d_c} {kw}: " + ", ".join(msg))
+
+
+TINY = LI.WORKLOADS["tiny_fp32"]
+V3 = LI.WORKLOADS["v3_shard_s4096"]
+
+
+@pytest.mark.parametrize("S,B,gamma,offset", [(256, 1, True, 0), (1, 1, True, 0), (7, 2, False, 0),
+                                              (257, 2, True, 1000), (100, 1, False, 123456789)])
+def test_tiny_fp32(S, B, gamma, offset):
+    check(TINY.replace(seq_len=S, batch=B), gamma=gamma, offset=offset)
+
+
+@pytest.mark.parametrize("S,H,B,gamma,offset", [(300, 16, 1, True, 0), (1, 1, 1, True, 0), (7, 3, 2, False, 0),
+                                                (16384, 16, 1, True, 0), (33, 5, 2, True, (1 << 31) + 5)])
+def test_v3_bf16(S, H, B, gamma, offset):
+    check(V3.replace(seq_len=S, n_heads=H, batch=B), gamma=gamma, offset=offset)
+
+
+def test_v3_fp32_mode_and_latent_width_extremes():
+    check(V3.replace(seq_len=333, n_heads=2, dtype="fp32"), gamma=True, offset=17)
+    check(V3.replace(seq_len=129, n_heads=2, d_c=1024), gamma=True)
+    check(V3.replace(seq_len=65, n_heads=1, d_c=32), gamma=True)
+
+
+def test_without_q_and_other_eps_and_base():
+    check(V3.replace(seq_len=70, n_heads=2), with_q=False, gamma=True)
+    check(TINY.replace(seq_len=50), eps=0.5, base=500.0, gamma=True)
+
+
+def test_in_place_contract_repeatability_and_head_shards():
+    import torch
+    import paper_2607_17644_amd as L
+    w = V3.replace(seq_len=257, n_heads=16)
+    x, _, (q, dq, d_gamma, d_lat) = run(w, gamma=True, offset=5)
+    # q_nope and dq_nope columns are untouched, bit for bit
+    q_in = to_dev(x["q"], w.dtype)
+    dq_in = to_dev(x["dq"], w.dtype)
+    assert torch.equal(q[..., :w.d_nope], q_in[..., :w.d_nope])
+    assert torch.equal(dq[..., :w.d_nope], dq_in[..., :w.d_nope])
+    # a second call gives the same bits (fixed-order d_gamma reduction)
+    _, _, (q2, dq2, d_gamma2, d_lat2) = run(w, gamma=True, offset=5)
+    assert torch.equal(q, q2) and torch.equal(dq, dq2) and torch.equal(d_gamma, d_gamma2)
+    assert torch.equal(d_lat, d_lat2)
+    # a 4-head shard rotates its heads' bands to the same bits as the 16-head call
+    ws = w.replace(n_heads=4)
+    ps = problem_for(ws)
+    qs = q_in[:, :, 4:8].contiguous()
+    L.laga_prologue_fwd(ps, to_dev(x["latent_raw"], w.dtype), to_dev(x["kpe_raw"], w.dtype), q=qs,
+                        gamma=to_dev(x["gamma"], w.dtype), position_offset=5)
+    torch.cuda.synchronize()
+    assert torch.equal(qs, q[:, :, 4:8])
+
+
+def test_backward_rotation_undoes_the_forward():
+    import torch
+    import paper_2607_17644_amd as L
+    w = TINY.replace(seq_len=300, batch=2)
+    x = LI.make_prologue_inputs(w)
+    p = problem_for(w)
+    q0 = to_dev(x["q"], "fp32")
+    q = q0.clone()
+    lat, kpe = to_dev(x["latent_raw"], "fp32"), to_dev(x["kpe_raw"], "fp32")
+    _, k_pe, rstd = L.laga_prologue_fwd(p, lat, kpe, q=q, position_offset=77)
+    dc = torch.zeros(p.shapes()["dc_kv"], dtype=torch.float32, device="cuda")
+    _, kpe_back, _ = L.laga_prologue_bwd(p, lat, rstd, dc, k_pe.float().contiguous(), dq=q, position_offset=77)
+    torch.cuda.synchronize()
+    assert float((q - q0).abs().max()) < 1e-5
+    assert float((kpe_back - kpe).abs().max()) < 1e-5
