@@ -7,7 +7,7 @@ import pytest
 
 import laga_inputs as LI
 from oracle import laga as O
-from _util import TOL, dev_inputs, f64, problem_for, scaled_err
+from _util import TOL, dev_inputs, err, f64, problem_for, scaled_err
 
 pytestmark = pytest.mark.gpu
 
@@ -57,3 +57,34 @@ def test_fused_workspace_and_limits():
     with pytest.raises(L.LagaError) as e:
         L.laga_attn_fwd(big, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"])
     assert e.value.status == 3
+
+
+@pytest.mark.parametrize("name,S,H,B,causal", [
+    ("tiny_fp32", 45, 4, 2, False), ("tiny_fp32", 100, 4, 1, True),
+    ("v3_shard_s4096", 300, 3, 2, True), ("v3_shard_s4096", 2048, 16, 1, True),
+    ("v3_shard_s4096", 65, 2, 1, False)])
+def test_fused_backward_equals_materialised_bitwise(name, S, H, B, causal):
+    """The backward in the fused mode (kv NULL: K/V rebuilt once into the workspace)
+    returns the materialised mode's gradients bit for bit, and they meet the oracle."""
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS[name].replace(seq_len=S, n_heads=H, batch=B, causal=causal)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    p = problem_for(w)
+    kv = L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"])
+    out, lse = L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv)
+    gm = L.laga_attn_bwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"])
+    pf = problem_for(w, kv_mode=L.KV_FUSED)
+    assert L.laga_workspace_bytes(pf, L.OP_BWD) > L.laga_workspace_bytes(p, L.OP_BWD)
+    gf = L.laga_attn_bwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], None, out, lse, d["dout"])
+    torch.cuda.synchronize()
+    names = ("dq", "dc_kv", "dk_pe", "dw_kv_b")
+    for n, a, b in zip(names, gm, gf):
+        assert torch.equal(a, b), n
+    ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], n_heads=H, d_nope=w.d_nope,
+                     d_v=w.d_v, scale=w.scale, causal=causal)
+    for n, g in zip(names, gf):
+        e = err(f64(g), ref[n]) if n == "dw_kv_b" else scaled_err(f64(g), ref[n])
+        tol = 3e-2 if (n == "dk_pe" and w.dtype == "bf16") else TOL[w.dtype]
+        assert e < tol, (n, e)

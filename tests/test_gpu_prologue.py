@@ -116,3 +116,49 @@ def test_backward_rotation_undoes_the_forward():
     torch.cuda.synchronize()
     assert float((q - q0).abs().max()) < 1e-5
     assert float((kpe_back - kpe).abs().max()) < 1e-5
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_chained_with_the_attention_block(dtype):
+    """Raw latent, k_pe and q -> producers -> up-projection + attention forward and backward
+    -> producers' backward, against the oracle chained the same way."""
+    import torch
+    import paper_2607_17644_amd as L
+    from oracle import laga as OL
+    w = V3.replace(seq_len=200, n_heads=3, batch=2, dtype=dtype)
+    x = LI.make_prologue_inputs(w)
+    # unit-scale latent rows here (rstd near 1): the producers' backward multiplies the
+    # attention block's dc_kv by rstd, which would scale its bf16 error by up to 10
+    lat = x["latent_raw"].astype(np.float64)
+    x["latent_raw"] = LI.round_to(lat / np.sqrt(np.mean(lat * lat, axis=-1, keepdims=True)), w.dtype)
+    a = LI.make_inputs(w)  # W_kv_b and dO for the attention block
+    p = problem_for(w)
+    dev = {k: to_dev(v, w.dtype if k not in ("dc_kv", "dk_pe") else "fp32") for k, v in x.items()}
+    W, dO = to_dev(a["w_kv_b"], w.dtype), to_dev(a["dout"], w.dtype)
+    q = dev["q"].clone()
+    c_kv, k_pe, rstd = L.laga_prologue_fwd(p, dev["latent_raw"], dev["kpe_raw"], q=q, gamma=dev["gamma"],
+                                           position_offset=3)
+    kv = L.laga_reconstruct_kv(p, c_kv, W)
+    out, lse = L.laga_attn_fwd(p, q, c_kv, k_pe, W, kv=kv)
+    dq, dc, dkpe, dw = L.laga_attn_bwd(p, q, c_kv, k_pe, W, kv, out, lse, dO)
+    d_lat, d_kpe, d_g = L.laga_prologue_bwd(p, dev["latent_raw"], rstd, dc, dkpe, dq=dq, gamma=dev["gamma"],
+                                            position_offset=3)
+    torch.cuda.synchronize()
+
+    rc, rk, rq, _ = O.prologue_forward(x["latent_raw"], x["kpe_raw"], x["q"], w.d_nope, x["gamma"],
+                                       position_offset=3)
+    kw = dict(n_heads=w.n_heads, d_nope=w.d_nope, d_v=w.d_v, scale=w.scale)
+    # the attention block receives the producers' outputs in the element dtype
+    rq, rc, rk = (LI.round_to(t, w.dtype) for t in (rq, rc, rk))
+    ro, _ = OL.attn_fwd(rq, rc, rk, a["w_kv_b"], **kw)
+    rg = OL.attn_bwd(rq, rc, rk, a["w_kv_b"], a["dout"], **kw)
+    rl, rkb, rqb, rgam = O.prologue_backward(x["latent_raw"], rg["dc_kv"], rg["dk_pe"], rg["dq"], w.d_nope,
+                                             x["gamma"], position_offset=3)
+    errs = {"out": scaled_err(f64(out), ro), "d_latent_raw": scaled_err(f64(d_lat), rl),
+            "d_kpe_raw": scaled_err(f64(d_kpe), rkb), "dq_raw": scaled_err(f64(dq), rqb),
+            "d_gamma": err(f64(d_g), rgam), "dw_kv_b": err(f64(dw), rg["dw_kv_b"])}
+    print(f"chained {dtype}: " + ", ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+    tol = TOL[w.dtype]
+    for k, v in errs.items():
+        # d_kpe_raw carries dk_pe's bf16 noise floor (the head sum at the first keys)
+        assert v < (1.5 * tol if (k == "d_kpe_raw" and dtype == "bf16") else tol), (k, v)
