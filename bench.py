@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=8,
                     help="heads of the workload the CPU oracle runs as its bounded sample")
+    ap.add_argument("--clock-probe", type=float, default=3.0, metavar="SECONDS",
+                    help="after the timed steps, run the step back to back this long while amd-smi "
+                         "samples the GFX clock and socket power (0: skip)")
     ap.add_argument("--fused-compare", action="store_true",
                     help="also time the forward with K/V rebuilt on chip (kv_mode=FUSED)")
     ap.add_argument("--pmc-probe", action="store_true",
@@ -158,7 +161,7 @@ def flops(w):
     return algorithmic_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
 
 
-def gpu_bench(w, steps, warmup, fused_compare):
+def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0):
     import torch
     import laga_inputs as LI
     import paper_2607_17644_amd as L
@@ -225,6 +228,8 @@ def gpu_bench(w, steps, warmup, fused_compare):
     assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
 
     res["prologue"] = prologue_bench(w, p, steps, warmup)
+    if clock_probe_s > 0:
+        res["clock"] = clock_under_load(step, clock_probe_s)
 
     if fused_compare:
         pf = L.Problem(**{**p.__dict__, "kv_mode": L.KV_FUSED})
@@ -244,6 +249,60 @@ def gpu_bench(w, steps, warmup, fused_compare):
             res["fused_fwd_ms"] = None
             res["fused_error"] = str(e)
     return res
+
+
+def clock_under_load(step, seconds):
+    """GFX clock and socket power (`amd-smi metric`, sampled in a side thread) while the
+    step runs back to back for `seconds`, after the timed steps: the clock the MFMA peak
+    is actually available at under this load. None if amd-smi is not available."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    import torch
+
+    exe = shutil.which("amd-smi")
+    if exe is None:
+        return None
+    raw = []
+    stop = threading.Event()
+
+    def sample():
+        while not stop.is_set():
+            try:
+                r = subprocess.run([exe, "metric", "-p", "-c", "-g", "0"], capture_output=True, text=True,
+                                   timeout=10)
+                raw.append(r.stdout)
+            except (OSError, subprocess.SubprocessError):
+                return
+            time.sleep(0.1)
+
+    step()
+    torch.cuda.synchronize()
+    th = threading.Thread(target=sample, daemon=True)
+    th.start()
+    t0, n = time.perf_counter(), 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            step()
+        n += 10
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    clk, pw = [], []
+    for out in raw[1:]:  # the first sample can straddle the start of the loop
+        pw += [float(v) for v in re.findall(r"SOCKET_POWER:\s*([0-9.]+)\s*W", out)]
+        clk += [float(v) for v in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*([0-9.]+)\s*MHz", out)]
+    if not clk:
+        return None
+
+    def med(v):
+        v = sorted(v)
+        return v[len(v) // 2]
+    ghz = med(clk) / 1e3
+    return {"gfx_clock_ghz_median": round(ghz, 3), "socket_power_w_median": med(pw) if pw else None,
+            "samples": len(raw) - 1, "steps": n, "seconds": round(time.perf_counter() - t0, 2),
+            "bf16_dense_peak_at_this_clock_tflops": round(PEAK_BF16_TFLOPS * ghz / 2.4, 1)}
 
 
 def prologue_bench(w, p, steps, warmup):
@@ -342,7 +401,7 @@ def main():
         pmc_probe(w)
         return
     fl = flops(w)
-    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare)
+    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare, a.clock_probe)
     ms = g["ms"]["step"]
     tflops = fl / (ms * 1e-3) / 1e12
 
@@ -381,6 +440,7 @@ def main():
         "roofline": roofline,
         "algorithmic_tflops_by_kernel": other,
         "prologue_outside_step": g.get("prologue"),
+        "clock_under_load": g.get("clock"),
         "cpu_baseline": cpu,
     }
     if a.fused_compare:
