@@ -114,3 +114,27 @@ def test_prologue_entry_points_validate_first():
     assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, z, fake, need, z) == 1
     assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, fake, fake, need - 1, z) == 5
     assert lib.laga_prologue_bwd(ctypes.byref(P.c()), ctypes.byref(cfg), *bargs, fake, z, need, z) == 5
+
+
+def test_workspace_sizes_follow_the_header():
+    """laga_workspace_bytes against the sizes include/laga.h states (host logic only)."""
+    lib, B = _raw()
+    for S, H, Bt in ((1, 1, 1), (64, 2, 1), (300, 3, 2), (16384, 16, 1)):
+        P = B.Problem(Bt, S, H, 512, 128, 64, 128)
+        T = (S + 31) // 32
+        ds = 2 * Bt * H * 512 * T * (T + 1)
+        dkv = 2 * Bt * S * H * 256
+        need = lib.laga_workspace_bytes(ctypes.byref(P.c()), 1)
+        # the dS^T store plus dKV hi and lo at least; everything rounded to 256 bytes
+        assert need >= ds + 2 * dkv and need % 256 == 0, (S, H, Bt)
+        # non-causal: the full square of tiles
+        Pn = B.Problem(Bt, S, H, 512, 128, 64, 128, causal=0)
+        assert lib.laga_workspace_bytes(ctypes.byref(Pn.c()), 1) - need == 2 * Bt * H * 1024 * T * T - ds
+        # the fused mode adds the rebuilt kv to the backward and W^T to the forward
+        Pf = B.Problem(Bt, S, H, 512, 128, 64, 128, kv_mode=B.KV_FUSED)
+        assert lib.laga_workspace_bytes(ctypes.byref(Pf.c()), 1) == need + dkv
+        assert lib.laga_workspace_bytes(ctypes.byref(Pf.c()), 0) == 2 * 512 * H * 256
+        assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 0) == 0
+    # fp32 stores no dS^T (4.3 GB in bf16 at S=16384, 16 heads): its workspace is linear in S
+    P = B.Problem(1, 16384, 16, 512, 128, 64, 128, dtype=B.DTYPE_FP32)
+    assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 1) < 1 << 30
