@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seq-len", type=int, default=None, help="override S (sweep); default 16384")
+    ap.add_argument("--heads", type=int, default=None,
+                    help="override the shard's head count (sweep over SP degrees); default 16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=8,
                     help="heads of the workload the CPU oracle runs as its bounded sample")
@@ -397,6 +399,8 @@ def main():
     w = LI.WORKLOADS[WORKLOAD]
     if a.seq_len:
         w = w.replace(seq_len=a.seq_len)
+    if a.heads:
+        w = w.replace(n_heads=a.heads)
     if a.pmc_probe:
         pmc_probe(w)
         return
@@ -412,7 +416,7 @@ def main():
     pairs = float(w.batch) * S * S / 2 * H
     dkdv_flops = pairs * 2 * (2 * w.d_v + w.d_qk)
     achieved = dkdv_flops / (g["ms"]["bwd_dkdv"] * 1e-3) / 1e12
-    traffic = stored_traffic() if a.seq_len is None else None
+    traffic = stored_traffic() if a.seq_len is None and a.heads is None else None
     roofline = {"kernel": TRAFFIC_KERNEL, "bound": "mfma", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic), "traffic_unit": "bytes per launch",
@@ -431,7 +435,8 @@ def main():
         "ms_per_step": round(ms, 4), "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; DeepSeek-V3 per-rank shapes)",
-        "config": {"workload": w.name if not a.seq_len else f"{w.name}@S={w.seq_len}", "seq_len": S,
+        "config": {"workload": w.name + (f"@S={w.seq_len}" if a.seq_len else "") + (f"@H={H}" if a.heads else ""),
+                   "seq_len": S,
                    "n_heads": H, "d_c": w.d_c, "d_nope": w.d_nope, "d_rope": w.d_rope, "d_v": w.d_v,
                    "batch": w.batch, "causal": True, "kv_mode": "materialised", "deterministic": True,
                    "algorithmic_gflop_per_step": round(fl / 1e9, 1)},
