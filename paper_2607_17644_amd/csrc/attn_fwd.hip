@@ -641,6 +641,14 @@ template <int DN, int DR, int DV> struct FwdTiles<float, DN, DR, DV> {
 
 }  // namespace
 
+// The bf16 forward picks its workgroup size by the grid it gives: 256 queries (fewer
+// re-reads of the K/V tiles) while that still yields this many workgroups (two per CU),
+// 128 below. Both sizes run the same per-wave computation in the same order, so results
+// do not depend on the choice. (The same rule for the key-stationary backward measured
+// slower with few heads: its longest workgroup, the first keys', sets the time whatever
+// its width.)
+constexpr int kFwdFillGroups = 512;
+
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   using Tl = FwdTiles<T, DN, DR, DV>;
@@ -655,10 +663,15 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
   dim3 grid(P.n_qblocks * P.n_hgroups, a.B, 1);
   if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128 && Tl::G == 1) {
     // 8 waves: 256 queries of one head per workgroup, which halves the K/V tile
-    // traffic of 4 waves (measured 8 % faster at S = 16384)
-    constexpr int RW = 8, RBR = 32 * RW;
-    P.n_qblocks = (a.S + RBR - 1) / RBR;
-    attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, RW><<<dim3(P.n_qblocks * P.n_hgroups, a.B, 1), 64 * RW, 0, st>>>(P);
+    // traffic of 4 waves (measured 8 % faster at S = 16384); 4 waves when 8 would leave
+    // fewer than kFwdFillGroups workgroups (few heads or short sequences)
+    auto ring = [&](auto rw) {
+      constexpr int RW = decltype(rw)::value, RBR = 32 * RW;
+      P.n_qblocks = (a.S + RBR - 1) / RBR;
+      attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, RW><<<dim3(P.n_qblocks * P.n_hgroups, a.B, 1), 64 * RW, 0, st>>>(P);
+    };
+    if ((long long)((a.S + 255) / 256) * P.n_hgroups * a.B >= kFwdFillGroups) ring(std::integral_constant<int, 8>{});
+    else ring(std::integral_constant<int, 4>{});
   } else {
     using Cfg = FwdCfg<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false>;
     attn_fwd_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH, Tl::G, false><<<grid, Cfg::NT, 0, st>>>(P);

@@ -128,6 +128,27 @@ def test_head_partition_bitwise(dtype):
     assert scaled_err(acc_dkpe, f64(full["dk_pe"])) < 1e-4
 
 
+def test_workgroup_size_choice_is_invisible():
+    """The forward takes 128 queries per workgroup instead of 256 when the grid would be
+    small: a 32-head run (256) and its 8-head shards (128) agree bit for bit, and so do
+    the gradients computed from them."""
+    import torch
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=4096, n_heads=32)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    full, out, lse = gpu_step(w, d)
+    ws = w.replace(n_heads=8)
+    for r in range(4):
+        hs = slice(r * 8, (r + 1) * 8)
+        ds = {"q": d["q"][:, :, hs].contiguous(), "c_kv": d["c_kv"], "k_pe": d["k_pe"],
+              "w_kv_b": d["w_kv_b"][:, r * 2048:(r + 1) * 2048].contiguous(),
+              "dout": d["dout"][:, :, hs].contiguous()}
+        g, o, l = gpu_step(ws, ds)
+        assert torch.equal(o, out[:, :, hs]) and torch.equal(l, lse[:, hs]), r
+        assert torch.equal(g["dq"], full["dq"][:, :, hs]), r
+        assert torch.equal(g["dw_kv_b"], full["dw_kv_b"][:, r * 2048:(r + 1) * 2048]), r
+
+
 def test_repeatable():
     import torch
     w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=700, n_heads=3)
