@@ -60,13 +60,18 @@ COPY_BYTES = 1 << 30  # bytes read and bytes written by the calibration copy
 
 
 def kernel_fingerprint():
-    """Hash of the sources the dominant kernel is built from: stored traffic is only
-    reported while they are unchanged."""
+    """Hash of the code (comments and blank lines removed) of the sources the dominant
+    kernel is built from: stored traffic is only reported while that code is unchanged."""
     import hashlib
+    import re
     hs = hashlib.sha256()
     for f in ("attn_bwd.hip", "common.hpp", "bwd_common.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2607_17644_amd", "csrc", f), "rb") as fh:
-            hs.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2607_17644_amd", "csrc", f)) as fh:
+            text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+        for line in text.splitlines():
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                hs.update(code.encode() + b"\n")
     return hs.hexdigest()[:16]
 
 

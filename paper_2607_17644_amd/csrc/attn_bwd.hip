@@ -279,10 +279,12 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 // Key-stationary backward with 16 keys per wave on the 16x16x32 MFMA: the per-wave
 // state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
 // the 32-key layout, so two waves share each SIMD and hide each other's latencies.
-// (Measured alternatives, both slower at S = 16384: 32 keys per wave on the 32x32x16
-// MFMA at one wave per SIMD, 4.5 ms; a pair of waves splitting 32 keys by product
-// (S/P/dV on one, dP/dZ/dK on the other, P exchanged through LDS), 4.7 ms; this
-// kernel, 3.3 ms.)
+// (Measured alternatives at S = 16384, this kernel 3.2-3.3 ms: 32 keys per wave on the
+// 32x32x16 MFMA at one wave per SIMD, 4.5 ms as a plain loop and 3.1-3.3 ms software-
+// pipelined with every LDS read at an immediate offset; a pair of waves splitting 32
+// keys into a K role and a V role, 3.1 ms. Those two read fewer LDS bytes per pair,
+// but in the whole step the other kernels then ran slower by as much, the board being
+// at its power limit.)
 // A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
 // (Q, dO, and lse2 / delta of the rows) stream through a two-stage LDS ring of direct
 // global->LDS loads into padded tiles (pitch = row + 2 chunks: conflict-free for both
