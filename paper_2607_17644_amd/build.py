@@ -61,7 +61,29 @@ def build(verbose: bool = False) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")
+    demo = build_c_consumer()
+    if verbose:
+        print(f"built {demo}")
     return LIB
+
+
+# A plain C program that uses only include/laga.h and the HIP runtime's C API (the GPU
+# tests run it to show that the boundary needs no PyTorch and no C++).
+C_DEMO_SRC = os.path.join(ROOT, "tests", "c_consumer", "laga_c_demo.c")
+C_DEMO = os.path.join(BUILD, "laga_c_demo")
+
+
+def build_c_consumer() -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(HIPCC)))
+    cmd = [os.environ.get("CC", "gcc"), "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror",
+           "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"), "-I", os.path.join(rocm, "include"),
+           C_DEMO_SRC, "-o", C_DEMO, "-L", PKG, "-llaga", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath," + os.path.join(rocm, "lib"), "-lm"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"C consumer build failed:\n{' '.join(cmd)}\n{r.stderr}")
+    return C_DEMO
 
 
 if __name__ == "__main__":
