@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=8,
                     help="heads of the workload the CPU oracle runs as its bounded sample")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip timing the step as one captured HIP graph")
     ap.add_argument("--clock-probe", type=float, default=3.0, metavar="SECONDS",
                     help="after the timed steps, run the step back to back this long while amd-smi "
                          "samples the GFX clock and socket power (0: skip)")
@@ -168,7 +170,7 @@ def flops(w):
     return algorithmic_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
 
 
-def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0):
+def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0, graph=False):
     import torch
     import laga_inputs as LI
     import paper_2607_17644_amd as L
@@ -198,17 +200,18 @@ def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0):
               ("bwd_finish", L.BWD_FINISH)]
     names = ["reconstruct_kv", "attn_fwd"] + [n for n, _ in stages]
 
-    def step(ev=None):
-        if ev: ev[0].record(stream)
-        L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"], kv=kv, stream=stream)
-        if ev: ev[1].record(stream)
+    def step(ev=None, on=None):
+        s = stream if on is None else on
+        if ev: ev[0].record(s)
+        L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"], kv=kv, stream=s)
+        if ev: ev[1].record(s)
         L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv, out=out, lse=lse,
-                        workspace=ws_f, stream=stream)
-        if ev: ev[2].record(stream)
+                        workspace=ws_f, stream=s)
+        if ev: ev[2].record(s)
         for i, (_, st) in enumerate(stages):
             L.laga_attn_bwd_stage(st, p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"],
-                                  dq, dc, dkpe, dw, ws_b, stream=stream)
-            if ev: ev[3 + i].record(stream)
+                                  dq, dc, dkpe, dw, ws_b, stream=s)
+            if ev: ev[3 + i].record(s)
 
     for _ in range(warmup):
         step()
@@ -234,6 +237,7 @@ def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0):
            "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
     assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
 
+    res["graph_ms_per_step"] = graph_step_ms(step, steps) if graph else None
     res["prologue"] = prologue_bench(w, p, steps, warmup)
     if clock_probe_s > 0:
         res["clock"] = clock_under_load(step, clock_probe_s)
@@ -256,6 +260,28 @@ def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0):
             res["fused_fwd_ms"] = None
             res["fused_error"] = str(e)
     return res
+
+
+def graph_step_ms(step, steps):
+    """The same step captured once in a HIP graph and replayed `steps` times (no host
+    launch work between the kernels): mean ms per replay."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            step(on=side)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
 
 
 def clock_under_load(step, seconds):
@@ -410,7 +436,7 @@ def main():
         pmc_probe(w)
         return
     fl = flops(w)
-    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare, a.clock_probe)
+    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare, a.clock_probe, graph=not a.no_graph)
     ms = g["ms"]["step"]
     tflops = fl / (ms * 1e-3) / 1e12
 
@@ -438,6 +464,7 @@ def main():
         "metric": "attention-block TFLOP/s and ms/step (fwd+bwd), S=16384, 16 heads, % bf16 MFMA peak",
         "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": round(ms, 4), "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "graph_ms_per_step": None if g["graph_ms_per_step"] is None else round(g["graph_ms_per_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; DeepSeek-V3 per-rank shapes)",
         "config": {"workload": w.name + (f"@S={w.seq_len}" if a.seq_len else "") + (f"@H={H}" if a.heads else ""),
