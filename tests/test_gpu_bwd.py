@@ -158,3 +158,47 @@ def test_repeatable():
     b, _, _ = gpu_step(w, d)
     for k in NAMES:
         assert torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_rising_scores_exercise_the_online_rescale(dtype):
+    """Scores that rise along the sequence (a shared direction added to k_pe with growing
+    weight, and to every q_rope) move each row's running maximum past its reference by more
+    than the lazy-rescale threshold several times, so the forward's O rescale runs at tile
+    boundaries all along the sweep; a larger q_nope makes the rows peaked. bf16: the
+    forward (where the rescale lives) against the oracle; its gradients at logits this far
+    from unit scale carry the bf16 rounding of dZ times the keys' large common component,
+    beyond the unit-scale bar, so the backward is checked in the fp32 mode."""
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=700, n_heads=3, dtype=dtype)
+    x = LI.make_inputs(w)
+    S = w.seq_len
+    u = np.zeros(w.d_rope); u[:2] = 1.0 / np.sqrt(2.0)
+    ramp = (np.arange(S, dtype=np.float64) / S)[None, :, None] * 40.0 * u  # q.k_pe gains up to 8 * 40
+    x["k_pe"] = LI.round_to(x["k_pe"].astype(np.float64) + ramp, dtype)
+    q = x["q"].astype(np.float64)
+    q[..., w.d_nope:] += 8.0 * u
+    q[..., :w.d_nope] *= 3.0
+    x["q"] = LI.round_to(q, dtype)
+    g, out, lse = gpu_step(w, dev_inputs(w, x))
+    ro, rl = O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **okw(w))
+    errs = {"out": scaled_err(f64(out), ro), "lse": scaled_err(f64(lse), rl)}
+    if dtype == "fp32":
+        ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+        errs.update({k: metric(k)(f64(g[k]), ref[k]) for k in NAMES})
+    print(f"rising scores {dtype}: lse range {rl.min():.1f}..{rl.max():.1f}; " +
+          " ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+    # the maximum over a row really moves by many rescale thresholds (2^8 in exp2 units)
+    assert (rl.max() - rl.min()) / np.log(2.0) > 3 * 8
+    for k, v in errs.items():
+        assert v < tol_for(k, w.dtype), (k, v)
+
+
+def test_random_shapes():
+    """Seeded random (B, S, H, causal) at the DeepSeek-V3 head dims, bf16, fwd + bwd."""
+    rng = np.random.default_rng(2026)
+    for _ in range(8):
+        S = int(rng.integers(1, 600))
+        H = int(rng.integers(1, 7))
+        B = int(rng.integers(1, 3))
+        causal = bool(rng.integers(0, 2))
+        check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal))
