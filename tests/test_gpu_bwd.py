@@ -72,14 +72,16 @@ def test_v3_fp32_mode():
     check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=300, n_heads=2, dtype="fp32"))
 
 
-def test_s16384_sampled():
-    """Training step at the per-rank shard (S=16384, 16 heads), as the benchmark runs it.
-    dq on sampled rows (row by row); dKV-derived rows dc_kv / dk_pe on the last keys, which
-    only see the last queries; dW through <W, dW> = <c_kv, dc_kv>; invariants."""
-    w = LI.WORKLOADS["v3_train_s16384"]
+@pytest.mark.parametrize("S", [16384, 16001])
+def test_s16384_sampled(S):
+    """Training step at the per-rank shard (S=16384, 16 heads), as the benchmark runs it,
+    and at a ragged length next to it. dq on sampled rows (row by row); dKV-derived rows
+    dc_kv / dk_pe on the last keys, which only see the last queries; dW through
+    <W, dW> = <c_kv, dc_kv>; invariants."""
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S)
     x = LI.make_inputs(w)
     g, out, _ = gpu_step(w, dev_inputs(w, x))
-    rows = [0, 1, 100, 5000, 16383]
+    rows = [0, 1, 100, 5000, S - 1]
     r = O.attn_fwd_rows(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], rows, dout=x["dout"],
                         n_heads=16, d_nope=128, d_v=128, scale=w.scale)
     assert scaled_err(f64(g["dq"][:, rows]), r["dq"]) < TOL["bf16"]
@@ -87,7 +89,7 @@ def test_s16384_sampled():
     rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
     for k in ("dq", "dc_kv", "dk_pe"):
         e = scaled_err(f64(g[k][:, tail:]), rb[k][:, tail:])
-        print(f"S=16384 tail rows {k}: {e:.3e}")
+        print(f"S={S} tail rows {k}: {e:.3e}")
         assert e < tol_for(k, "bf16"), (k, e)
     check_invariants(x, g)
 
