@@ -204,3 +204,26 @@ def test_random_shapes():
         B = int(rng.integers(1, 3))
         causal = bool(rng.integers(0, 2))
         check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal))
+
+
+def test_s16384_two_heads_against_the_full_oracle():
+    """The benchmark's configuration (S=16384, 16 heads) against the full oracle on two of
+    its heads: dq and the dW columns of heads 0-1 of the 16-head run (they depend on their
+    own head only), and dc_kv / dk_pe of the 2-head shard (its partial sums), every element."""
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_train_s16384"]
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    g16, _, _ = gpu_step(w, d)
+    w2 = w.replace(n_heads=2)
+    x2 = {"q": x["q"][:, :, :2], "c_kv": x["c_kv"], "k_pe": x["k_pe"], "w_kv_b": x["w_kv_b"][:, :512],
+          "dout": x["dout"][:, :, :2]}
+    g2, _, _ = gpu_step(w2, dev_inputs(w2, x2))
+    ref = O.attn_bwd(x2["q"], x2["c_kv"], x2["k_pe"], x2["w_kv_b"], x2["dout"], **okw(w2))
+    errs = {"dq": scaled_err(f64(g16["dq"][:, :, :2]), ref["dq"]),
+            "dw_kv_b": err(f64(g16["dw_kv_b"][:, :512]), ref["dw_kv_b"]),
+            "dc_kv": scaled_err(f64(g2["dc_kv"]), ref["dc_kv"]),
+            "dk_pe": scaled_err(f64(g2["dk_pe"]), ref["dk_pe"])}
+    print("S=16384 heads 0-1 vs the full oracle: " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+    for k, v in errs.items():
+        assert v < tol_for(k, "bf16"), (k, v)
