@@ -115,3 +115,17 @@ def test_repeatable_and_prefix():
           "k_pe": d["k_pe"][:, :512].contiguous(), "w_kv_b": d["w_kv_b"]}
     op, lp = gpu_fwd(wp, dp)
     assert torch.equal(op, o1[:, :512]) and torch.equal(lp, l1[:, :, :512])
+
+
+def test_s16384_two_heads_every_row():
+    """The benchmark's configuration (S=16384, 16 heads): out and lse of heads 0-1, every
+    row, against the full oracle on those two heads."""
+    w = LI.WORKLOADS["v3_shard_s16384"]
+    x = LI.make_inputs(w, with_dout=False)
+    out, lse = gpu_fwd(w, dev_inputs(w, x))
+    w2 = w.replace(n_heads=2)
+    x2 = {"q": x["q"][:, :, :2], "c_kv": x["c_kv"], "k_pe": x["k_pe"], "w_kv_b": x["w_kv_b"][:, :512]}
+    ro, rl = oracle_fwd(w2, x2)
+    eo, el = err(f64(out[:, :, :2]), ro), err(f64(lse[:, :2]), rl)
+    print(f"S=16384 heads 0-1, every row: out {eo:.2e} lse {el:.2e}")
+    assert eo < TOL["bf16"] and el < TOL["bf16"]
