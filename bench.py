@@ -56,8 +56,8 @@ def parse():
 
 
 # HBM traffic of the dominant kernel, from counters (see --pmc-probe / --summarize-pmc).
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dkdv16_kernel_v3_train_s16384_hbm_traffic.txt")
-TRAFFIC_KERNEL = "dkdv16_kernel"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dkdv32_kernel_v3_train_s16384_hbm_traffic.txt")
+TRAFFIC_KERNEL = "dkdv32_kernel"
 COPY_BYTES = 1 << 30  # bytes read and bytes written by the calibration copy
 
 

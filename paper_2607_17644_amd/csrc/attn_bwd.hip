@@ -20,6 +20,9 @@
 //                  query layout (S^T = K Q^T), dQ^T += K^T dZ^T with K^T read by
 //                  transposing LDS reads; it recomputes S and dP (the price of
 //                  not accumulating dQ with atomics)
+//   dkdv32_kernel  the same for bf16 with 192/128-wide heads, 32 keys per wave on
+//                  the 32x32x16 MFMA, software-pipelined (see there); it also
+//                  stores dS^T for the dQ pass
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
 #include <type_traits>
 
@@ -276,42 +279,41 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 }
 
 
-// Key-stationary backward with 16 keys per wave on the 16x16x32 MFMA: the per-wave
-// state (K and V rows 40 registers, dK^T / dV^T accumulators 80) is half that of
-// the 32-key layout, so two waves share each SIMD and hide each other's latencies.
-// (Measured alternatives at S = 16384, this kernel 3.2-3.3 ms: 32 keys per wave on the
-// 32x32x16 MFMA at one wave per SIMD, 4.5 ms as a plain loop and 3.1-3.3 ms software-
-// pipelined with every LDS read at an immediate offset; a pair of waves splitting 32
-// keys into a K role and a V role, 3.1 ms. Those two read fewer LDS bytes per pair,
-// but in the whole step the other kernels then ran slower by as much, the board being
-// at its power limit.)
-// A workgroup of WPH waves owns 16 * WPH keys of one head; query tiles of 32 rows
-// (Q, dO, and lse2 / delta of the rows) stream through a two-stage LDS ring of direct
-// global->LDS loads into padded tiles (pitch = row + 2 chunks: conflict-free for both
-// 16x16 read patterns, and every read is a per-lane base address plus a constant).
-//   S = Q K^T, dP = dO V^T: A = Q / dO rows (16-byte row fragments), B = the lane's
-//       key / value row; accumulator: lane <-> key, 4 queries per 16-query block.
-//   dV^T += dO^T P, dK^T += Q^T dZ: the contraction over the tile's 32 queries takes
-//       P / dZ straight from the accumulators in the order {4G..4G+3, 16+4G..16+4G+3}
-//       (G = lane / 16), matched by two transposing 4-row reads of dO / Q.
-// Alongside, dS^T = dZ (bf16) is stored for the dQ pass.
-template <int DN, int DR, int DV, int WPH, int NS>
-__global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
+// Key-stationary dK/dV for bf16 with 192/128-wide heads: 32 keys per wave on the
+// 32x32x16 MFMA, one wave per SIMD (4 waves, 128 keys per workgroup). The wave's K and V
+// rows (A operands) and its dK^T / dV^T accumulators stay in registers for the whole
+// sweep (about 450 registers with the pipeline below); a 32x32x16 fragment read from LDS
+// feeds 32 Kflop, so per (query, key) pair the kernel reads half the LDS bytes of a
+// 16-key layout. Per 32-query tile t:
+//   A(t): S = Q K^T, dP = dO V^T        20 MFMAs on Q / dO row fragments
+//   B(t): P = exp2(S c - lse2), dZ = P (dP - delta), the dS^T store    VALU
+//   C(t): dV^T += dO^T P, dK^T += Q^T dZ  20 MFMAs on transposing reads of dO / Q
+// With no second wave on its SIMD to hide latencies, the wave overlaps B(t-1) with A(t)
+// (the softmax of one tile beside the MFMAs of the next; S and dP of consecutive tiles
+// alternate between two accumulator sets), then runs C(t-1); the instruction order is
+// fixed with sched_barrier, LDS reads issued three MFMAs ahead, each exponential one
+// slot before the product that uses it. Query tiles (Q, dO, and each wave's copy of
+// the tile's lse2 / delta rows) stream through a four-slot LDS ring of direct
+// global->LDS loads into XOR-swizzled tiles, two tiles ahead. Every wave sweeps all of
+// the workgroup's tiles (those before its own keys run fully masked and add exact
+// zeros), so a tile's ring slot is the same in every wave: the loop is unrolled over
+// the four slots and every LDS read is a per-lane base register plus an immediate
+// offset, with no address arithmetic in the loop. The per-wave issue rate, not the LDS,
+// is then its limit. It also stores dZ (bf16) as dS^T for the dQ pass.
+template <int DN, int DR, int DV>
+__global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   using T = bf16;
-  constexpr int DQK = DN + DR, DKVH = DN + DV, BQ = 32, NW = WPH, BK = 16 * WPH;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = 4, BK = 32 * NW, BQ = 32, NS = 4;
   constexpr int QCPR = DQK / 8, OCPR = DV / 8;
-  static_assert(QCPR % 4 == 0 && OCPR % 4 == 0, "padded pitches assume rows of whole 64-byte groups");
-  static_assert(NS == 2, "two-stage ring (the waits are full vmcnt waits)");
-  constexpr int QP = QCPR + 2, OP = OCPR + 2;  // pitches in chunks, P % 4 == 2
-  constexpr int NQI = pad_chunks(BQ, QP) / 64, NOI = pad_chunks(BQ, OP) / 64;
-  static_assert(NQI * 64 == BQ * QP && NOI * 64 == BQ * OP, "tiles are whole load instructions");
-  // ring stages as distinct LDS objects (so the compiler does not make the reads of one
-  // stage wait for the direct loads into another); unused stages are not allocated
-  __shared__ __attribute__((aligned(16))) T sQ0[NQI * 512], sQ1[NQI * 512], sQ2[NQI * 512], sQ3[NQI * 512];
-  __shared__ __attribute__((aligned(16))) T sO0[NOI * 512], sO1[NOI * 512], sO2[NOI * 512], sO3[NOI * 512];
-  // lse2 of the tile's rows, then delta (the load instruction covers 1 KB; lanes 16..63
-  // repeat lanes 0..15)
-  __shared__ __attribute__((aligned(16))) float sL0[256], sL1[256], sL2[256], sL3[256];
+  static_assert(QCPR == 24 && OCPR == 16, "swizzles are defined for 192/128-wide rows");
+  constexpr int QCH = BQ * QCPR, OCH = BQ * OCPR;
+  constexpr int KQ = QCH / 64 / NW, KO = OCH / 64 / NW;
+  static_assert(KQ * 64 * NW == QCH && KO * 64 * NW == OCH && 5 * (KQ + KO) <= 32, "load split");
+  constexpr int F = KQ + KO + 1;
+  constexpr int QTB = QCH * 16, OTB = OCH * 16;  // tile bytes
+  __shared__ __attribute__((aligned(16))) T sQ[NS][QCH * 8];
+  __shared__ __attribute__((aligned(16))) T sO[NS][OCH * 8];
+  __shared__ __attribute__((aligned(16))) float sL[NS][NW][256];
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -325,217 +327,319 @@ __global__ __launch_bounds__(64 * WPH) void dkdv16_kernel(BwdParams P) {
   const int bh = lin / P.n_blocks;
   const int b = bh / H, h = bh % H;
 
-  const int tid = threadIdx.x, l = tid & 63, j = l & 15, G = l >> 4;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);  // uniform, known < NW
-  const int k0 = kb * BK + wave * 16;
-  const int my_k = k0 + j;
+  const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);
+  const int k0 = kb * BK + wave * 32;
+  const int my_k = k0 + n;
+  const bool key_ok = my_k < S;
+  const size_t krow = (size_t)(b * S + (key_ok ? my_k : 0));
+  const int q_lo = P.causal ? my_k : 0;
+  const unsigned q_span = key_ok ? (unsigned)(S - q_lo) : 0u;
 
-  bf16x8 kf[DQK / 32], vf[DV / 32];
-  {
-    const bool ok = my_k < S;
-    const size_t row = (size_t)(b * S + (ok ? my_k : 0));
-    const T* kvr = kv + (row * H + h) * DKVH;
+  const int qt_begin = P.causal ? kb * BK : 0;
+  const int ntiles = (S - qt_begin + BQ - 1) / BQ;
+
+  const size_t hrow0 = (size_t)(b * S) * H + h;
+  uint32_t qoff[KQ], ooff[KO], rows = 0;
 #pragma unroll
-    for (int ks = 0; ks < DQK / 32; ++ks) {
-      const int d = ks * 32 + G * 8;
-      const T* src = d < DN ? kvr + d : kpe + row * DR + (d - DN);
-      kf[ks] = *reinterpret_cast<const bf16x8*>(src);
-      if (!ok) kf[ks] = bf16x8{};
-    }
-#pragma unroll
-    for (int ks = 0; ks < DV / 32; ++ks) {
-      vf[ks] = *reinterpret_cast<const bf16x8*>(kvr + DN + ks * 32 + G * 8);
-      if (!ok) vf[ks] = bf16x8{};
-    }
+  for (int k = 0; k < KQ; ++k) {
+    const int p = (wave + k * NW) * 64 + l, r = p / QCPR, c = (p % QCPR) ^ swz<QCPR>(r);
+    qoff[k] = 2u * (r * H * DQK + c * 8);
+    rows |= (uint32_t)r << (5 * k);
   }
-
-  f32x4 dk[DQK / 16], dv[DV / 16];
 #pragma unroll
-  for (int i = 0; i < DQK / 16; ++i) dk[i] = f32x4{};
-#pragma unroll
-  for (int i = 0; i < DV / 16; ++i) dv[i] = f32x4{};
-
-  // Loads of a tile: Q chunks (instruction js of NQI goes to wave js % NW), dO chunks
-  // likewise, and the lse2 / delta rows in one instruction of wave NW - 1. Each lane
-  // keeps its source pointer for the tile at query 0, and a tile adds qt rows (one
-  // 64-bit add); which instructions a wave issues is fixed, so the dispatch is a few
-  // scalar compares. A tile crossing the end of the data (rows past S, clamped to
-  // S - 1; their P is masked) takes a slower path.
-  constexpr int KQ = (NQI + NW - 1) / NW, KO = (NOI + NW - 1) / NW;
-  auto q_chunk = [&](int js, int rmax) {  // element offset of this lane's Q chunk from row 0
-    const int p = js * 64 + l, r = min(p / QP, rmax), c = p % QP;
-    return r * H * DQK + (c < QCPR ? c : 0) * 8;
-  };
-  auto o_chunk = [&](int js, int rmax) {
-    const int p = js * 64 + l, r = min(p / OP, rmax), c = p % OP;
-    return r * H * DV + (c < OCPR ? c : 0) * 8;
-  };
-  const size_t hrow0 = (size_t)(b * S) * H + h;  // row (b, 0, h)
-  const T* qlane[KQ];
-  const T* olane[KO];
-#pragma unroll
-  for (int k = 0; k < KQ; ++k) qlane[k] = q + hrow0 * DQK + q_chunk(wave + k * NW, BQ - 1);
-#pragma unroll
-  for (int k = 0; k < KO; ++k) olane[k] = dout + hrow0 * DV + o_chunk(wave + k * NW, BQ - 1);
-  const float* llane = (j < 8 ? P.lse2 : P.delta) + (size_t)(b * H + h) * P.S_pad + 4 * (j & 7);
-
-  auto fill = [&](T* tq, T* to, float* tl, int qt) {
-    const size_t qstep = (size_t)qt * H;
+  for (int k = 0; k < KO; ++k) {
+    const int p = (wave + k * NW) * 64 + l, r = p / OCPR, c = (p % OCPR) ^ swz<OCPR>(r);
+    ooff[k] = 2u * (r * H * DV + c * 8);
+    rows |= (uint32_t)r << (5 * (KQ + k));
+  }
+  const float* llane = ((l & 15) < 8 ? P.lse2 : P.delta) + (size_t)bh * P.S_pad + 4 * (l & 7);
+  auto fill = [&](int st, int qt) {
+    const T* qb = q + (hrow0 + (size_t)qt * H) * DQK;
+    const T* ob = dout + (hrow0 + (size_t)qt * H) * DV;
     if (qt + BQ <= S) {
 #pragma unroll
-      for (int k = 0; k < KQ; ++k)
-        if (wave + k * NW < NQI) g2lds16(qlane[k] + qstep * DQK, tq + (wave + k * NW) * 512);
+      for (int k = 0; k < KQ; ++k) g2lds16_so(qb, qoff[k], &sQ[st][(wave + k * NW) * 512]);
 #pragma unroll
-      for (int k = 0; k < KO; ++k)
-        if (wave + k * NW < NOI) g2lds16(olane[k] + qstep * DV, to + (wave + k * NW) * 512);
+      for (int k = 0; k < KO; ++k) g2lds16_so(ob, ooff[k], &sO[st][(wave + k * NW) * 512]);
     } else {
-      const T* qb = q + (hrow0 + qstep) * DQK;
-      const T* ob = dout + (hrow0 + qstep) * DV;
+      const int rmax = S - 1 - qt;
 #pragma unroll
-      for (int k = 0; k < KQ; ++k)
-        if (wave + k * NW < NQI) g2lds16(qb + q_chunk(wave + k * NW, S - 1 - qt), tq + (wave + k * NW) * 512);
+      for (int k = 0; k < KQ; ++k) {
+        const int over = max((int)((rows >> (5 * k)) & 31u) - rmax, 0);
+        g2lds16_so(qb, qoff[k] - 2u * over * H * DQK, &sQ[st][(wave + k * NW) * 512]);
+      }
 #pragma unroll
-      for (int k = 0; k < KO; ++k)
-        if (wave + k * NW < NOI) g2lds16(ob + o_chunk(wave + k * NW, S - 1 - qt), to + (wave + k * NW) * 512);
-    }
-    if (wave == NW - 1) g2lds16(llane + qt, tl);
-  };
-
-  // dS^T of a tile for the dQ pass: key my_k's row of 32 queries; the lane holds
-  // queries {4G..4G+3} and {16+4G..16+4G+3}. Only the keys the tile sees are stored.
-  // The store of tile i is issued right after the barrier of tile i + 1, so its
-  // latency hides behind a whole tile. dsl: this key's row in query tile 0.
-  T* const dsl = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, 0) + (size_t)my_k * BQ;
-  bf16x8 zs{};
-  int ts = -1;
-  auto store_ds = [&]() {
-    if (ts >= 0 && my_k < ds_tile_keys(P.ds_T, P.causal, ts)) {
-      T* dsr = dsl + (P.causal ? (size_t)512 * ts * (ts + 1) : (size_t)1024 * P.ds_T * ts);
-      *reinterpret_cast<bf16x4*>(dsr + 4 * G) = __builtin_shufflevector(zs, zs, 0, 1, 2, 3);
-      *reinterpret_cast<bf16x4*>(dsr + 16 + 4 * G) = __builtin_shufflevector(zs, zs, 4, 5, 6, 7);
-    }
-  };
-
-  // live (query, key) pairs of this lane's key: q_lo <= query < q_lo + q_span (none
-  // for keys past S), tested with one unsigned compare
-  const int q_lo = P.causal ? my_k : 0;
-  const unsigned q_span = my_k < S ? (unsigned)(S - q_lo) : 0u;
-
-  const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
-  const int ntiles = (S - qt_begin + BQ - 1) / BQ;
-  auto stage_q = [&](auto st) -> T* {
-    constexpr int X = decltype(st)::value;
-    return X == 0 ? sQ0 : X == 1 ? sQ1 : X == 2 ? sQ2 : sQ3;
-  };
-  auto stage_o = [&](auto st) -> T* {
-    constexpr int X = decltype(st)::value;
-    return X == 0 ? sO0 : X == 1 ? sO1 : X == 2 ? sO2 : sO3;
-  };
-  auto stage_l = [&](auto st) -> float* {
-    constexpr int X = decltype(st)::value;
-    return X == 0 ? sL0 : X == 1 ? sL1 : X == 2 ? sL2 : sL3;
-  };
-  {
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    fill(stage_q(I0{}), stage_o(I0{}), stage_l(I0{}), qt_begin);
-    if (NS > 2 && ntiles > 1) fill(stage_q(I1{}), stage_o(I1{}), stage_l(I1{}), qt_begin + BQ);
-    if (NS > 3 && ntiles > 2) fill(stage_q(I2{}), stage_o(I2{}), stage_l(I2{}), qt_begin + 2 * BQ);
-  }
-  auto step = [&](auto stage, int it) {
-    constexpr int ST = decltype(stage)::value;
-    using NX = std::integral_constant<int, (ST + NS - 1) % NS>;
-    const int qt = qt_begin + it * BQ;
-    // this wave's loads of tile `it` have landed: in the steady state exactly the
-    // NS - 2 later tiles' loads may still be in flight
-    wait_vmem();
-    __syncthreads();  // ... and everyone's; the stage filled next (read at it - 1) is free
-    store_ds();       // tile it - 1
-    if (it + NS - 1 < ntiles) fill(stage_q(NX{}), stage_o(NX{}), stage_l(NX{}), qt + (NS - 1) * BQ);
-    const T* tq = stage_q(stage);
-    const T* to = stage_o(stage);
-    const float* tld = stage_l(stage);
-    // masked: queries past S, keys past S (their dS is stored as zeros) and, causally,
-    // keys after the query
-    const bool need_mask = (P.causal && qt < k0 + 15) || (qt + BQ > S) || (k0 + 16 > S);
-
-    f32x4 sa[2], dp[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      sa[qb] = f32x4{};
-      dp[qb] = f32x4{};
-#pragma unroll
-      for (int ks = 0; ks < DQK / 32; ++ks) mma16(sa[qb], pad_frag<QP>(tq, qb * 16 + j, 4 * ks + G), kf[ks]);
-#pragma unroll
-      for (int ks = 0; ks < DV / 32; ++ks) mma16(dp[qb], pad_frag<OP>(to, qb * 16 + j, 4 * ks + G), vf[ks]);
-    }
-    if (need_mask) {
-      asm volatile("");  // keep the branch: the common unmasked tile runs no mask code
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          sa[qb][e] = (unsigned)(qt + qb * 16 + G * 4 + e - q_lo) < q_span ? sa[qb][e] : -INFINITY;
-    }
-    bf16x8 pf, zf;
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int qrow = qb * 16 + G * 4;
-      const f32x4 lq = *reinterpret_cast<const f32x4*>(tld + qrow);
-      const f32x4 dq = *reinterpret_cast<const f32x4*>(tld + BQ + qrow);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float p = fast_exp2(__builtin_fmaf(sa[qb][e], P.scale_log2, -lq[e]));
-        pf[qb * 4 + e] = to_elem<T>(p);
-        zf[qb * 4 + e] = to_elem<T>(p * (dp[qb][e] - dq[e]));
+      for (int k = 0; k < KO; ++k) {
+        const int over = max((int)((rows >> (5 * (KQ + k))) & 31u) - rmax, 0);
+        g2lds16_so(ob, ooff[k] - 2u * over * H * DV, &sO[st][(wave + k * NW) * 512]);
       }
     }
-    zs = zf;
-    ts = qt / BQ;
-    const int ra = 4 * G, rb = 16 + 4 * G;
-#pragma unroll
-    for (int db = 0; db < DV / 16; ++db) mma16(dv[db], pad_tr_frag16<OP>(to, ra, rb, db * 16), pf);
-#pragma unroll
-    for (int db = 0; db < DQK / 16; ++db) mma16(dk[db], pad_tr_frag16<QP>(tq, ra, rb, db * 16), zf);
+    g2lds16(llane + qt, sL[st][wave]);
   };
-  for (int it = 0; it < ntiles; it += NS) {
-    step(std::integral_constant<int, 0>{}, it);
-    if (it + 1 < ntiles) step(std::integral_constant<int, 1 % NS>{}, it + 1);
-    if (NS > 2 && it + 2 < ntiles) step(std::integral_constant<int, 2 % NS>{}, it + 2);
-    if (NS > 3 && it + 3 < ntiles) step(std::integral_constant<int, 3 % NS>{}, it + 3);
-  }
-  store_ds();  // the last tile
 
-  if (my_k >= S) return;
-  const size_t row = (size_t)(b * S + my_k) * H + h;
+  frag_t<T> kf[DQK / 16], vf[DV / 16];
+  {
+    const T* kvr = kv + (krow * H + h) * DKVH;
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      const T* src = ks < DN / 16 ? kvr + ks * 16 + 8 * g : kpe + krow * DR + (ks - DN / 16) * 16 + 8 * g;
+      kf[ks] = *reinterpret_cast<const frag_t<T>*>(src);
+      if (!key_ok) kf[ks] = frag_t<T>{};
+    }
+#pragma unroll
+    for (int ks = 0; ks < DV / 16; ++ks) {
+      vf[ks] = *reinterpret_cast<const frag_t<T>*>(kvr + DN + ks * 16 + 8 * g);
+      if (!key_ok) vf[ks] = frag_t<T>{};
+    }
+  }
+  f32x16 dk[DQK / 32], dv[DV / 32];
+#pragma unroll
+  for (int i = 0; i < DQK / 32; ++i) dk[i] = f32x16{};
+#pragma unroll
+  for (int i = 0; i < DV / 32; ++i) dv[i] = f32x16{};
+
+  // per-lane LDS addresses inside slot 0 of each ring (laundered through an empty asm so
+  // that the compiler keeps one register per base and folds slot and step offsets into
+  // the reads' immediate offsets); other slots and steps are immediates
+  typedef __attribute__((address_space(3))) const char* lptr;
+  typedef __attribute__((address_space(3))) const frag_t<T> lfrag;
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  auto base = [](const void* arr, uint32_t off) {
+    lptr p = (lptr)(const char*)arr + off;
+    asm volatile("" : "+v"(p));
+    return p;
+  };
+  lptr Qr[4], Qa[2], Qbo[2], Or[DV / 16], Oa[DV / 32], Obo[DV / 32];
+  {
+    const int s16 = l & 15, ra = 4 * g + (s16 >> 2), rb = ra + 8;
+    const int lc = 2 * ((l >> 4) & 1) + ((s16 & 3) >> 1), e4 = 4 * (s16 & 1);
+    const int sq = swz<QCPR>(n), so = swz<OCPR>(n);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Qr[j] = base(sQ, 2u * (n * DQK + ((2 * j + g) ^ sq) * 8));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      Qa[j] = base(sQ, 2u * (ra * DQK + ((4 * j + lc) ^ swz<QCPR>(ra)) * 8 + e4));
+      Qbo[j] = base(sQ, 2u * (rb * DQK + ((4 * j + lc) ^ swz<QCPR>(rb)) * 8 + e4));
+    }
+#pragma unroll
+    for (int ks = 0; ks < DV / 16; ++ks) Or[ks] = base(sO, 2u * (n * DV + ((2 * ks + g) ^ so) * 8));
+#pragma unroll
+    for (int db = 0; db < DV / 32; ++db) {
+      Oa[db] = base(sO, 2u * (ra * DV + ((4 * db + lc) ^ swz<OCPR>(ra)) * 8 + e4));
+      Obo[db] = base(sO, 2u * (rb * DV + ((4 * db + lc) ^ swz<OCPR>(rb)) * 8 + e4));
+    }
+  }
+  auto tr = [](lptr pa, lptr pb) {
+    const bf16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)pa);
+    const bf16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)pb);
+    return __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  auto rowq = [&](int st, int ks) { return *(lfrag*)(Qr[ks & 3] + (st * QTB + (ks >> 2) * 128)); };
+  auto rowo = [&](int st, int ks) { return *(lfrag*)(Or[ks] + st * OTB); };
+  // C operand i of tile slot st: query half kk = i / 10; blocks 0..5 of dK^T, then 0..3 of dV^T
+  auto c_read = [&](int st, int i) {
+    const int kk = i / 10, m = i % 10;
+    if (m < DQK / 32) {
+      const int c = st * QTB + kk * 16 * DQK * 2 + (m >> 1) * 128;
+      return tr(Qa[m & 1] + c, Qbo[m & 1] + c);
+    }
+    const int db = m - DQK / 32, c = st * OTB + kk * 16 * DV * 2;
+    return tr(Oa[db] + c, Obo[db] + c);
+  };
+  auto step_a = [&](int st, f32x16& sa, f32x16& dp) {
+    sa = f32x16{};
+    dp = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < DQK / 16; ++ks) {
+      mma(sa, rowq(st, ks), kf[ks]);
+      if (ks < DV / 16) mma(dp, rowo(st, ks), vf[ks]);
+    }
+  };
+  auto mask_b = [&](int j, f32x16& sa) {
+    const int qt = qt_begin + j * BQ;
+    if ((P.causal && qt < k0 + 31) || qt + BQ > S || k0 + 32 > S) {
+      asm volatile("");
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sa[r] = (unsigned)(qt + (r >> 2) * 8 + g * 4 + (r & 3) - q_lo) < q_span ? sa[r] : -INFINITY;
+    }
+  };
+  auto step_b = [&](int st, const f32x16& sa, const f32x16& dp, bf16x8 (&pf)[2], bf16x8 (&zf)[2]) {
+    const float* tl = sL[st][wave];
+    f32x16 p, z;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const f32x4 lq = *reinterpret_cast<const f32x4*>(tl + rr * 8 + g * 4);
+      const f32x4 dq = *reinterpret_cast<const f32x4*>(tl + BQ + rr * 8 + g * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[rr * 4 + e] = fast_exp2(__builtin_fmaf(sa[rr * 4 + e], P.scale_log2, -lq[e]));
+        z[rr * 4 + e] = p[rr * 4 + e] * (dp[rr * 4 + e] - dq[e]);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < BQ / 16; ++kk) {
+      pf[kk] = acc_to_frag<T>(p, kk);
+      zf[kk] = acc_to_frag<T>(z, kk);
+    }
+  };
+  T* const dsw = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, 0) + (size_t)k0 * BQ;
+  auto store_ds = [&](int j, const bf16x8 (&zf)[2]) {
+    const int t = (qt_begin + j * BQ) / BQ;
+    if (my_k < ds_tile_keys(P.ds_T, P.causal, t)) {
+      T* dsr = dsw + (P.causal ? (size_t)512 * t * (t + 1) : (size_t)1024 * P.ds_T * t) + (n * BQ + g * 4);
+#pragma unroll
+      for (int kk = 0; kk < BQ / 16; ++kk) {
+        *reinterpret_cast<bf16x4*>(dsr + kk * 16) = __builtin_shufflevector(zf[kk], zf[kk], 0, 1, 2, 3);
+        *reinterpret_cast<bf16x4*>(dsr + kk * 16 + 8) = __builtin_shufflevector(zf[kk], zf[kk], 4, 5, 6, 7);
+      }
+    }
+  };
+  auto sync = [&](int j) {
+    if (j + 1 < ntiles) wait_vmem_le<F>();
+    else wait_vmem();
+    lds_barrier();
+    if (j + 2 < ntiles) fill((j + 2) % NS, qt_begin + (j + 2) * BQ);
+  };
+
+  fill(0, qt_begin);
+  if (ntiles > 1) fill(1, qt_begin + BQ);
+  f32x16 sa0, dp0, sa1, dp1;
+  bf16x8 pf[2], zf[2];
+  sync(0);
+  step_a(0, sa0, dp0);
+  constexpr int PF = 3;
+  // step of tile jj (slot K = jj % 4): B(jj - 1) beside A(jj), then C(jj - 1)
+  auto step = [&](auto kc, int jj) {
+    constexpr int K = decltype(kc)::value;
+    constexpr int ST = K, SP = (K + NS - 1) % NS, ODD = K & 1;
+    f32x16& sa_a = ODD ? sa1 : sa0;
+    f32x16& dp_a = ODD ? dp1 : dp0;
+    f32x16& sa_b = ODD ? sa0 : sa1;
+    f32x16& dp_b = ODD ? dp0 : dp1;
+    sync(jj);
+    mask_b(jj - 1, sa_b);
+    const float* tl = sL[SP][wave];
+    f32x4 lq[4], dq[4];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      lq[rr] = *reinterpret_cast<const f32x4*>(tl + rr * 8 + g * 4);
+      dq[rr] = *reinterpret_cast<const f32x4*>(tl + BQ + rr * 8 + g * 4);
+    }
+    auto a_is_s = [](int i) { return i >= 16 || (i & 1) == 0; };
+    auto a_ks = [](int i) { return i >= 16 ? 8 + (i - 16) : i >> 1; };
+    auto a_read = [&](int i) { return a_is_s(i) ? rowq(ST, a_ks(i)) : rowo(ST, a_ks(i)); };
+    frag_t<T> ab[PF + 1];
+#pragma unroll
+    for (int i = 0; i < PF; ++i) ab[i] = a_read(i);
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 p, z;
+#pragma unroll
+    for (int i = 0; i < 20; ++i) {
+      if (i + PF < 20) ab[(i + PF) % (PF + 1)] = a_read(i + PF);
+      if (a_is_s(i))
+        sa_a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[i % (PF + 1)], kf[a_ks(i)], i == 0 ? f32x16{} : sa_a,
+                                                       0, 0, 0);
+      else
+        dp_a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[i % (PF + 1)], vf[a_ks(i)], i == 1 ? f32x16{} : dp_a,
+                                                       0, 0, 0);
+      // softmax element i (exp issued one slot before its product)
+      if (i < 16) p[i] = fast_exp2(__builtin_fmaf(sa_b[i], P.scale_log2, -lq[i >> 2][i & 3]));
+      if (i >= 1 && i <= 16) z[i - 1] = p[i - 1] * (dp_b[i - 1] - dq[(i - 1) >> 2][(i - 1) & 3]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int kk = 0; kk < BQ / 16; ++kk) {
+      pf[kk] = acc_to_frag<T>(p, kk);
+      zf[kk] = acc_to_frag<T>(z, kk);
+    }
+    bf16x8 cb[PF + 1];
+#pragma unroll
+    for (int i = 0; i < PF; ++i) cb[i] = c_read(SP, i);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 20; ++i) {
+      if (i + PF < 20) cb[(i + PF) % (PF + 1)] = c_read(SP, i + PF);
+      const int kk = i / 10, m = i % 10;
+      if (m < DQK / 32) mma(dk[m], cb[i % (PF + 1)], zf[kk]);
+      else mma(dv[m - DQK / 32], cb[i % (PF + 1)], pf[kk]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    store_ds(jj - 1, zf);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  {
+    int j = 1;
+    for (; j + 3 < ntiles; j += 4) {
+      step(I1{}, j);
+      step(I2{}, j + 1);
+      step(I3{}, j + 2);
+      step(I0{}, j + 3);
+    }
+    if (j < ntiles) step(I1{}, j++);
+    if (j < ntiles) step(I2{}, j++);
+    if (j < ntiles) step(I3{}, j++);
+  }
+  // the last tile's B and C (its slot and parity are not known at compile time)
+  {
+    const int jl = ntiles - 1, sl = jl % NS;
+    if (jl & 1) {
+      mask_b(jl, sa1);
+      step_b(sl, sa1, dp1, pf, zf);
+    } else {
+      mask_b(jl, sa0);
+      step_b(sl, sa0, dp0, pf, zf);
+    }
+#pragma unroll
+    for (int i = 0; i < 20; ++i) {
+      const int kk = i / 10, m = i % 10;
+      if (m < DQK / 32) mma(dk[m], c_read(sl, i), zf[kk]);
+      else mma(dv[m - DQK / 32], c_read(sl, i), pf[kk]);
+    }
+    store_ds(jl, zf);
+  }
+
+  if (!key_ok) return;
+  const size_t row = krow * H + h;
   T* dkvr = (T*)P.dkv + row * DKVH;
   T* dkvl = (T*)P.dkv_lo + row * DKVH;
   float* dper = P.dkpe_h + row * DR;
-  auto put4 = [&](int col, const f32x4& a, float sc) {
+  auto put = [&](int col, const f32x4& v) {
     bf16x4 hi, lo;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float x = a[e] * sc;
-      hi[e] = to_elem<T>(x);
-      lo[e] = to_elem<T>(x - to_f32(hi[e]));
+      hi[e] = to_elem<T>(v[e]);
+      lo[e] = to_elem<T>(v[e] - to_f32(hi[e]));
     }
     *reinterpret_cast<bf16x4*>(dkvr + col) = hi;
     *reinterpret_cast<bf16x4*>(dkvl + col) = lo;
   };
 #pragma unroll
-  for (int db = 0; db < DQK / 16; ++db) {
-    const int d = db * 16 + G * 4;
-    if (d < DN) {
-      put4(d, dk[db], P.scale);
-    } else {
-      f32x4 v = dk[db] * P.scale;
-      *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
-    }
-  }
+  for (int db = 0; db < DQK / 32; ++db)
 #pragma unroll
-  for (int db = 0; db < DV / 16; ++db) put4(DN + db * 16 + G * 4, dv[db], 1.f);
+    for (int rr = 0; rr < 4; ++rr) {
+      const int d = db * 32 + rr * 8 + g * 4;
+      f32x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = dk[db][4 * rr + e] * P.scale;
+      if (d >= DN) *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
+      else put(d, v);
+    }
+#pragma unroll
+  for (int db = 0; db < DV / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      f32x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = dv[db][4 * rr + e];
+      put(DN + db * 32 + rr * 8 + g * 4, v);
+    }
 }
+
 
 // dk_pe[b,t,:] = sum_{h ascending} dkpe_h[b,t,h,:]   (one thread per 4 outputs, fp32)
 template <int DR>
@@ -567,12 +671,8 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
                                                       a.S, a.S_pad, a.H, BS);
   } else if (stage == 1) {
     if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
-      // two stages: three and four measured 25 % and 17 % slower at S = 16384 (the
-      // loads are mostly cache hits that one tile of compute covers; more stages cost
-      // code size and scalar registers)
-      constexpr int WPH16 = 8, BK = 16 * WPH16, NS = 2;
-      P.n_blocks = (a.S + BK - 1) / BK;
-      dkdv16_kernel<DN, DR, DV, WPH16, NS><<<dim3(P.n_blocks * a.H, a.B), 64 * WPH16, 0, st>>>(P);
+      P.n_blocks = (a.S + 127) / 128;
+      dkdv32_kernel<DN, DR, DV><<<dim3(P.n_blocks * a.H, a.B), 256, 0, st>>>(P);
     } else {
       constexpr int BK = 32 * Tl::WPH_KV;
       P.n_blocks = (a.S + BK - 1) / BK;

@@ -252,39 +252,6 @@ __device__ __forceinline__ bf16x8 swz_tr_frag(const bf16* tile, int ra, int rb, 
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
-// 16x16x32 bf16 MFMA (one 16x16 output block, contraction over 32): lane l serves
-// row/column (l % 16) of its operand and contraction indices 8 * (l / 16) .. +7;
-// its 4 accumulators hold output column (l % 16) at rows 4 * (l / 16) + e.
-__device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8& b) {
-  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-}
-
-// Direct global->LDS fill of a swizzled tile of NROWS x CPR chunks by NW waves:
-// wave instruction j covers physical chunks [64 j, 64 j + 64); lane i fetches the
-// logical chunk that belongs at physical chunk 64 j + i, i.e. c = p ^ swz(row), from
-// chunk_ptr(row, c) (the address of that chunk's first element). chunk_ptr must
-// return a valid address for every row (callers clamp rows past the end of the
-// data; those rows are masked later).
-template <typename T, int NROWS, int CPR, int NW, typename ChunkPtr>
-__device__ __forceinline__ void swz_fill_chunks(T* tile, int wave, int l, ChunkPtr chunk_ptr) {
-  constexpr int E = 16 / sizeof(T);
-  constexpr int N = NROWS * CPR;
-  static_assert(N % 64 == 0, "tile must be whole wave instructions");
-#pragma unroll
-  for (int j = wave; j < N / 64; j += NW) {
-    const int p = j * 64 + l;
-    const int row = p / CPR, c = (p % CPR) ^ swz<CPR>(row);
-    g2lds16(chunk_ptr(row, c), tile + j * 64 * E);
-  }
-}
-
-// Same, for tiles whose rows are contiguous in global memory: row_ptr(row) + 16 * c bytes.
-template <typename T, int NROWS, int CPR, int NW, typename RowPtr>
-__device__ __forceinline__ void swz_fill(T* tile, int wave, int l, RowPtr row_ptr) {
-  constexpr int E = 16 / sizeof(T);
-  swz_fill_chunks<T, NROWS, CPR, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
-}
-
 // ---------------------------------------------------------------- padded tiles
 // A "padded tile" holds NROWS rows of CPR 16-byte chunks at a pitch of P chunks (P - CPR
 // chunks of padding at the end of each row). Unlike an XOR swizzle, padding keeps every
@@ -320,93 +287,12 @@ __device__ __forceinline__ void pad_fill_chunks(T* tile, int wave, int l, ChunkP
   }
 }
 
-// Same, for tiles whose rows are contiguous in global memory: row_ptr(row) + 16 * c bytes.
-template <typename T, int NROWS, int CPR, int P, int NW, typename RowPtr>
-__device__ __forceinline__ void pad_fill(T* tile, int wave, int l, RowPtr row_ptr) {
-  constexpr int E = 16 / sizeof(T);
-  pad_fill_chunks<T, NROWS, CPR, P, NW>(tile, wave, l, [&](int row, int c) { return row_ptr(row) + c * E; });
-}
-
-// Padded-tile fill with the per-lane address arithmetic done once: the tile's rows
-// sit at a fixed element stride in global memory; chunks c < NSPLIT of row r come from
-// base0 + r * stride0 + 8 c, chunks c >= NSPLIT (if any) from base1 + r * stride1 +
-// 8 (c - NSPLIT). init() stores, for each of this wave's load instructions, the lane's
-// element offset (and which source it reads); fill() then costs one 64-bit add per
-// instruction. Only a tile that crosses the end of the data (rows_valid < NROWS) takes
-// the slower path that clamps rows to rows_valid - 1. Same chunk assignment as
-// pad_fill_chunks.
-template <typename T, int NROWS, int CPR, int P, int NW, int NSPLIT = CPR>
-struct PadFill {
-  static constexpr int E = 16 / sizeof(T);
-  static constexpr int NI = pad_chunks(NROWS, P) / 64;
-  static constexpr int K = (NI + NW - 1) / NW;  // most instructions any wave issues
-  int off[K];
-  int second;  // bit k: instruction k reads the second source
-  __device__ __forceinline__ void locate(int wave, int l, int k, int rmax, int& r, int& c) const {
-    const int p = (wave + k * NW) * 64 + l;
-    r = p / P;
-    c = p % P;
-    if (r >= NROWS) r = 0;
-    if (c >= CPR) c = 0;
-    r = min(r, rmax);
-  }
-  __device__ __forceinline__ void init(int wave, int l, int stride0, int stride1) {
-    second = 0;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      int r, c;
-      locate(wave, l, k, NROWS - 1, r, c);
-      const bool s1 = c >= NSPLIT;
-      off[k] = s1 ? r * stride1 + (c - NSPLIT) * E : r * stride0 + c * E;
-      second |= (int)s1 << k;
-    }
-  }
-  __device__ __forceinline__ void fill(T* tile, int wave, int l, const T* base0, const T* base1, int stride0,
-                                       int stride1, int rows_valid) const {
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int j = wave + k * NW;
-      if (j >= NI) break;  // wave-uniform
-      const bool s1 = (second >> k) & 1;
-      int o = off[k];
-      if (rows_valid < NROWS) {  // wave-uniform; the last tile only
-        int r, c;
-        locate(wave, l, k, rows_valid - 1, r, c);
-        o = s1 ? r * stride1 + (c - NSPLIT) * E : r * stride0 + c * E;
-      }
-      g2lds16((s1 ? base1 : base0) + o, tile + j * 64 * E);
-    }
-  }
-};
-
-// 16-byte row fragment: chunk c of `row` of a padded bf16 tile.
-template <int P>
-__device__ __forceinline__ bf16x8 pad_frag(const bf16* tile, int row, int c) {
-  return *reinterpret_cast<const bf16x8*>(tile + (row * P + c) * 8);
-}
-
 // Transposing fragment (32x32x16 lane layout, see TrRead) from a padded bf16 tile of
 // pitch P chunks: lane l gets X[ra + e][c0 + l%32] and X[rb + e][c0 + l%32], e = 0..3.
 template <int P>
 __device__ __forceinline__ bf16x8 pad_tr_frag(const bf16* tile, int ra, int rb, int c0) {
   const int l = threadIdx.x & 63, s = l & 15;
   const int col = c0 + 16 * ((l >> 4) & 1) + 4 * (s & 3);
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  const bf16* pa = tile + (ra + (s >> 2)) * P * 8 + col;
-  const bf16* pb = tile + (rb + (s >> 2)) * P * 8 + col;
-  bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pa));
-  bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(pb));
-  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// Transposing fragment for the 16x16x32 shape from a padded bf16 tile: every 16-lane
-// group reads the same 16 columns c0 .. c0+15; lane l returns X[ra + e][c0 + l%16]
-// (e = 0..3) and X[rb + e][c0 + l%16] (e = 0..3), ra and rb per lane (they normally
-// depend on the group l / 16), both multiples of 4.
-template <int P>
-__device__ __forceinline__ bf16x8 pad_tr_frag16(const bf16* tile, int ra, int rb, int c0) {
-  const int s = threadIdx.x & 15;
-  const int col = c0 + 4 * (s & 3);
   typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
   const bf16* pa = tile + (ra + (s >> 2)) * P * 8 + col;
   const bf16* pb = tile + (rb + (s >> 2)) * P * 8 + col;
