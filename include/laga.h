@@ -50,6 +50,12 @@
  *   - Supported head dims: (d_nope, d_rope, d_v) = (128, 64, 128) — DeepSeek-V3 —
  *     and (32, 16, 32); d_c a multiple of 32 up to 1024; S >= 1; B >= 1; H >= 1.
  *     Anything else returns LAGA_ERR_UNSUPPORTED.
+ *   - Kernels index inside a tensor with 32-bit element offsets: B*S*H*W, with
+ *     W = d_nope + max(d_rope, d_v) + max(d_nope, d_v), B*S*d_c, B*S, and
+ *     16*d_c*H*(d_nope + d_v) must each stay below 2^31, else
+ *     LAGA_ERR_UNSUPPORTED (and laga_workspace_bytes() returns 0). Memory,
+ *     not this limit, bounds S first for the backward: its dS^T store holds
+ *     B*H*S*S/2 bf16 values.
  *   - Results do not depend on H: every per-head output (kv columns, out, lse,
  *     dq, dw_kv_b columns) of a head is bit-identical whichever head shard it is
  *     computed in; with deterministic = 1 repeated calls are bit-identical.

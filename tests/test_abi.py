@@ -61,6 +61,14 @@ def test_validation_errors_without_launch():
                        ("causal", 2), ("deterministic", 5), ("reserved", 1)):
         Q = B.Problem(**{**P.__dict__, field: val})
         assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 3, field
+    # 32-bit element offsets: the largest tensor must stay below 2^31 elements
+    s_max = ((1 << 31) - 1) // (16 * 384)
+    for S, H, code in ((s_max + 1, 16, 3), (1 << 31, 1, 3)):
+        Q = B.Problem(**{**P.__dict__, "seq_len": S, "n_heads": H})
+        assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == code, (S, H)
+        assert lib.laga_workspace_bytes(ctypes.byref(Q.c()), 1) == 0
+    Q = B.Problem(**{**P.__dict__, "seq_len": s_max, "n_heads": 16})
+    assert lib.laga_workspace_bytes(ctypes.byref(Q.c()), 1) > 0  # the largest accepted size
     # misaligned
     assert lib.laga_reconstruct_kv(ctypes.byref(P.c()), vp(0x10008), fake, fake, None) == 4
     # workspace sizes: forward needs none in materialised mode, backward some
