@@ -94,6 +94,28 @@ def test_s16384_sampled(S):
     check_invariants(x, g)
 
 
+def test_long_sequence_two_heads():
+    """S = 65536 with two heads: each head's dS^T store holds 2^31 bf16 values, so the
+    second head and the late query tiles sit past 32-bit element offsets. Sampled dq
+    rows, the tail rows of dq / dc_kv / dk_pe, and the invariants."""
+    S = 65536
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=2)
+    x = LI.make_inputs(w)
+    g, out, _ = gpu_step(w, dev_inputs(w, x))
+    rows = [0, 33, 40000, S - 33, S - 1]
+    r = O.attn_fwd_rows(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], rows, dout=x["dout"], **okw(w))
+    e = scaled_err(f64(g["dq"][:, rows]), r["dq"])
+    print(f"S={S} sampled dq rows: {e:.3e}")
+    assert e < TOL["bf16"]
+    tail = S - 96
+    rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
+    for k in ("dq", "dc_kv", "dk_pe"):
+        e = scaled_err(f64(g[k][:, tail:]), rb[k][:, tail:])
+        print(f"S={S} tail rows {k}: {e:.3e}")
+        assert e < tol_for(k, "bf16"), (k, e)
+    check_invariants(x, g)
+
+
 def check_invariants(x, g):
     """Exact identities (P6) evaluated on the GPU's gradients, at bf16-level tolerance."""
     dk_pe, dc, dw = f64(g["dk_pe"]), f64(g["dc_kv"]), f64(g["dw_kv_b"])
