@@ -165,9 +165,18 @@ def pmc_probe(w):
     gpu_bench(w, 1, 1, False)
 
 
+def step_flops(B, S, H, d_c, d_qk, d_v, d_kvh):
+    """Algorithmic flops of one step (forward + backward), causal pairs counted as S^2/2:
+    the up-projection 2 B S d_c H d_kvh forward and twice that backward; attention
+    forward (Q K^T and P V) B S^2 H (d_qk + d_v) and backward (dV, dP, dQ, dK) twice
+    that. The backward's recomputation of Q K^T is not counted."""
+    up = 2.0 * B * S * d_c * H * d_kvh
+    att = float(B) * S * S * H * (d_qk + d_v)
+    return 3.0 * up + 3.0 * att
+
+
 def flops(w):
-    from oracle.laga import algorithmic_flops  # pure arithmetic helper, no oracle compute
-    return algorithmic_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
+    return step_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
 
 
 def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0, graph=False):
@@ -396,7 +405,6 @@ def cpu_baseline(w, heads):
     import numpy as np
     import laga_inputs as LI
     from oracle import laga as O
-    from oracle.laga import algorithmic_flops
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
@@ -409,7 +417,7 @@ def cpu_baseline(w, heads):
     O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **kw)
     O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **kw)
     dt = time.perf_counter() - t0
-    f = algorithmic_flops(ws.batch, ws.seq_len, heads, ws.d_c, ws.d_qk, ws.d_v, ws.d_kvh)
+    f = step_flops(ws.batch, ws.seq_len, heads, ws.d_c, ws.d_qk, ws.d_v, ws.d_kvh)
     return {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"oracle fp64 numpy fwd+bwd (bwd recomputes the forward) of {heads} of {w.n_heads} "
                       f"heads at S={w.seq_len}: {f / 1e9:.1f} GFLOP in {dt:.1f} s",
