@@ -430,7 +430,7 @@ def main():
         summarize_pmc(*a.summarize_pmc)
         return
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the per-rank block has no "
+        print(json.dumps({"error": "the benchmark runs on one GPU only: the per-rank block has no "
                           "inter-GPU step (the collectives around it are out of scope); "
                           "run with --gpus 1"}))
         sys.exit(2)
