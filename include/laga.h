@@ -82,7 +82,7 @@ typedef enum {
   LAGA_OK = 0,
   LAGA_ERR_NULL = 1,        /* a required pointer (or the problem) is NULL */
   LAGA_ERR_SHAPE = 2,       /* a dimension is <= 0 or sizes are inconsistent */
-  LAGA_ERR_UNSUPPORTED = 3, /* dims/dtype/mode this build has no kernel for */
+  LAGA_ERR_UNSUPPORTED = 3, /* dims/dtype/mode/size the library has no kernel for */
   LAGA_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
   LAGA_ERR_WORKSPACE = 5,   /* workspace smaller than laga_workspace_bytes() */
   LAGA_ERR_DEVICE = 6       /* the HIP runtime reported an error at launch */

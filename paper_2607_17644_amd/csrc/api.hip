@@ -129,7 +129,7 @@ const char* laga_status_string(laga_status_t s) {
     case LAGA_OK: return "LAGA_OK: success";
     case LAGA_ERR_NULL: return "LAGA_ERR_NULL: a required pointer is NULL";
     case LAGA_ERR_SHAPE: return "LAGA_ERR_SHAPE: a dimension is not positive or the scale is not finite and positive";
-    case LAGA_ERR_UNSUPPORTED: return "LAGA_ERR_UNSUPPORTED: head dims, d_c, dtype, mode or size not supported by this build";
+    case LAGA_ERR_UNSUPPORTED: return "LAGA_ERR_UNSUPPORTED: head dims, d_c, dtype, mode or size not supported by this library";
     case LAGA_ERR_ALIGN: return "LAGA_ERR_ALIGN: a pointer is not 16-byte aligned";
     case LAGA_ERR_WORKSPACE: return "LAGA_ERR_WORKSPACE: workspace smaller than laga_workspace_bytes()";
     case LAGA_ERR_DEVICE: return "LAGA_ERR_DEVICE: the HIP runtime reported a launch error";
