@@ -488,12 +488,10 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   auto store_ds = [&](int j, const bf16x8 (&zf)[2]) {
     const int t = (qt_begin + j * BQ) / BQ;
     if (my_k < ds_tile_keys(P.ds_T, P.causal, t)) {
-      T* dsr = dsw + (P.causal ? (size_t)512 * t * (t + 1) : (size_t)1024 * P.ds_T * t) + (n * BQ + g * 4);
+      // accumulator element r of this lane is query 8 (r / 4) + 4 g + r % 4: position 16 g + r
+      T* dsr = dsw + (P.causal ? (size_t)512 * t * (t + 1) : (size_t)1024 * P.ds_T * t) + (n * BQ + g * 16);
 #pragma unroll
-      for (int kk = 0; kk < BQ / 16; ++kk) {
-        *reinterpret_cast<bf16x4*>(dsr + kk * 16) = __builtin_shufflevector(zf[kk], zf[kk], 0, 1, 2, 3);
-        *reinterpret_cast<bf16x4*>(dsr + kk * 16 + 8) = __builtin_shufflevector(zf[kk], zf[kk], 4, 5, 6, 7);
-      }
+      for (int kk = 0; kk < BQ / 16; ++kk) *reinterpret_cast<bf16x8*>(dsr + kk * 8) = zf[kk];
     }
   };
   auto sync = [&](int j) {

@@ -264,7 +264,8 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
     if (it + 3 < ntiles) step(std::integral_constant<int, 3>{}, it + 3);
   }
 
-  const int my_q = t * 32 + n;
+  // accumulator column n holds the query stored at position n of the dS^T rows
+  const int my_q = t * 32 + ds_query_of_position(n);
   if (!wave_ok || my_q >= S) return;
   T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll

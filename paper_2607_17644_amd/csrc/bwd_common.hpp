@@ -45,7 +45,13 @@ struct BwdParams {
 
 // dS^T store layout: for every (b, h) and query tile t of 32 rows, the keys that tile
 // sees (32 (t + 1) with the causal mask, 32 T without) as rows of 32 bf16 values, one
-// per query of the tile (key-major, 64-byte rows). Keys past S hold zeros.
+// per query of the tile (key-major, 64-byte rows). Keys past S hold zeros. Within a row,
+// query 8j + 4g + e (j < 4, g < 2, e < 4) sits at position 16g + 4j + e: the 16 queries
+// one lane of the dK/dV kernel holds in its accumulator (column layout of the 32x32
+// MFMA) are contiguous, so it writes them as two 16-byte stores.
+__host__ __device__ constexpr int ds_query_of_position(int pos) {
+  return 8 * ((pos >> 2) & 3) + 4 * (pos >> 4) + (pos & 3);
+}
 __host__ __device__ inline size_t ds_head_elems(int T, int causal) {
   return causal ? (size_t)512 * T * (T + 1) : (size_t)1024 * T * T;
 }
