@@ -488,10 +488,12 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   auto store_ds = [&](int j, const bf16x8 (&zf)[2]) {
     const int t = (qt_begin + j * BQ) / BQ;
     if (my_k < ds_tile_keys(P.ds_T, P.causal, t)) {
-      // accumulator element r of this lane is query 8 (r / 4) + 4 g + r % 4: position 16 g + r
+      // accumulator element r of this lane is query 8 (r / 4) + 4 g + r % 4: position 16 g + r.
+      // Non-temporal: the store is read back only by the dQ pass, long after this kernel.
       T* dsr = dsw + (P.causal ? (size_t)512 * t * (t + 1) : (size_t)1024 * P.ds_T * t) + (n * BQ + g * 16);
 #pragma unroll
-      for (int kk = 0; kk < BQ / 16; ++kk) *reinterpret_cast<bf16x8*>(dsr + kk * 8) = zf[kk];
+      for (int kk = 0; kk < BQ / 16; ++kk)
+        __builtin_nontemporal_store(zf[kk], reinterpret_cast<bf16x8*>(dsr + kk * 8));
     }
   };
   auto sync = [&](int j) {
