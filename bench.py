@@ -9,6 +9,12 @@ already resident in HBM. Prints ONE JSON line (see --help).
 Metric: algorithmic TFLOP/s of the step (causal pairs counted as S^2/2;
 attention fwd 320*S^2*H, bwd 640*S^2*H, up-projection 3 x 2*S*d_c*H*256),
 ms per step, and the fraction of the MI355X dense bf16 MFMA peak.
+
+Beside the headline step (dq from the stored dS^T), the same line reports the step with
+dq recomputed (no S x S buffer), the step with K/V rebuilt on chip from the latent
+(kv_mode FUSED; the forward's executed and algorithmic TFLOP/s), the step at
+S = 2048, 4096 and 8192, the producers around the all-gather, the clock under load and
+the CPU oracle (fp32 timed, fp64 beside it) on a bounded sample of the workload.
 """
 from __future__ import annotations
 
@@ -37,15 +43,16 @@ def parse():
     ap.add_argument("--heads", type=int, default=None,
                     help="override the shard's head count (sweep over SP degrees); default 16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=8,
+    ap.add_argument("--cpu-heads", type=int, default=4,
                     help="heads of the workload the CPU oracle runs as its bounded sample")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip timing the step as one captured HIP graph")
     ap.add_argument("--clock-probe", type=float, default=3.0, metavar="SECONDS",
                     help="after the timed steps, run the step back to back this long while amd-smi "
                          "samples the GFX clock and socket power (0: skip)")
-    ap.add_argument("--fused-compare", action="store_true",
-                    help="also time the forward with K/V rebuilt on chip (kv_mode=FUSED)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the default step: skip the dq-recompute and fused K/V modes, the "
+                         "S sweep (2048, 4096, 8192) and the producers")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: a plain copy kernel of known size (the HBM byte "
                          "counters' calibration), then one warm-up and one measured step; prints nothing")
@@ -162,7 +169,7 @@ def pmc_probe(w):
     torch.mul(src, 1.0, out=dst)  # the calibration copy: reads and writes COPY_BYTES
     torch.cuda.synchronize()
     del src, dst
-    gpu_bench(w, 1, 1, False)
+    gpu_bench(w, 1, 1, extras=False)
 
 
 def step_flops(B, S, H, d_c, d_qk, d_v, d_kvh):
@@ -179,96 +186,147 @@ def flops(w):
     return step_flops(w.batch, w.seq_len, w.n_heads, w.d_c, w.d_qk, w.d_v, w.d_kvh)
 
 
-def gpu_bench(w, steps, warmup, fused_compare, clock_probe_s=0.0, graph=False):
-    import torch
-    import laga_inputs as LI
-    import paper_2607_17644_amd as L
+def _median(v):
+    v = sorted(v)
+    return v[len(v) // 2] if len(v) % 2 else 0.5 * (v[len(v) // 2 - 1] + v[len(v) // 2])
 
-    x = LI.make_inputs(w)
-    dev = torch.device("cuda:0")
-    d = {k: torch.from_numpy(v).to(torch.bfloat16).to(dev) for k, v in x.items()}
-    p = L.Problem(batch=w.batch, seq_len=w.seq_len, n_heads=w.n_heads, d_c=w.d_c, d_nope=w.d_nope,
-                  d_rope=w.d_rope, d_v=w.d_v, softmax_scale=w.scale, causal=1, dtype=L.DTYPE_BF16,
-                  kv_mode=L.KV_MATERIALIZED, deterministic=1)
-    sh = p.shapes()
-    bf, f32 = torch.bfloat16, torch.float32
-    kv = torch.empty(sh["kv"], dtype=bf, device=dev)
-    out = torch.empty(sh["out"], dtype=bf, device=dev)
-    lse = torch.empty(sh["lse"], dtype=f32, device=dev)
-    dq = torch.empty(sh["dq"], dtype=bf, device=dev)
-    dc = torch.empty(sh["dc_kv"], dtype=f32, device=dev)
-    dkpe = torch.empty(sh["dk_pe"], dtype=f32, device=dev)
-    dw = torch.empty(sh["dw_kv_b"], dtype=f32, device=dev)
-    ws_f = torch.empty(max(1, L.laga_workspace_bytes(p, L.OP_FWD)), dtype=torch.uint8, device=dev)
-    ws_b = torch.empty(max(1, L.laga_workspace_bytes(p, L.OP_BWD)), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream(dev)
 
-    # the backward runs as its four stages (exactly what laga_attn_bwd does) so that each
-    # stage's kernels can be timed with events on the stream they are launched on
-    stages = [("bwd_prepare", L.BWD_PREPARE), ("bwd_dkdv", L.BWD_DKDV), ("bwd_dq", L.BWD_DQ),
-              ("bwd_finish", L.BWD_FINISH)]
-    names = ["reconstruct_kv", "attn_fwd"] + [n for n, _ in stages]
+class StepRunner:
+    """Device inputs, outputs and workspaces of one problem, and its step: laga_reconstruct_kv
+    (materialised K/V only) + laga_attn_fwd + the four stages of laga_attn_bwd, each entry
+    point bracketed by HIP events recorded on the stream it is launched on."""
 
-    def step(ev=None, on=None):
-        s = stream if on is None else on
+    def __init__(self, w, kv_mode=0, dq_mode=0, x=None):
+        import torch
+        import laga_inputs as LI
+        import paper_2607_17644_amd as L
+        self.L, self.w = L, w
+        x = LI.make_inputs(w) if x is None else x
+        dev = torch.device("cuda:0")
+        self.d = {k: torch.from_numpy(v).to(torch.bfloat16).to(dev) for k, v in x.items()}
+        self.p = L.Problem(batch=w.batch, seq_len=w.seq_len, n_heads=w.n_heads, d_c=w.d_c, d_nope=w.d_nope,
+                           d_rope=w.d_rope, d_v=w.d_v, softmax_scale=w.scale, causal=1, dtype=L.DTYPE_BF16,
+                           kv_mode=kv_mode, deterministic=1, dq_mode=dq_mode)
+        self.fused = kv_mode == L.KV_FUSED
+        sh = self.p.shapes()
+        bf, f32 = torch.bfloat16, torch.float32
+        e = lambda n, dt: torch.empty(sh[n], dtype=dt, device=dev)
+        self.kv = None if self.fused else e("kv", bf)
+        self.out, self.lse, self.dq = e("out", bf), e("lse", f32), e("dq", bf)
+        self.dc, self.dkpe, self.dw = e("dc_kv", f32), e("dk_pe", f32), e("dw_kv_b", f32)
+        self.ws_bytes = {"fwd": L.laga_workspace_bytes(self.p, L.OP_FWD), "bwd": L.laga_workspace_bytes(self.p, L.OP_BWD)}
+        self.ws_f = torch.empty(max(1, self.ws_bytes["fwd"]), dtype=torch.uint8, device=dev)
+        self.ws_b = torch.empty(max(1, self.ws_bytes["bwd"]), dtype=torch.uint8, device=dev)
+        self.stream = torch.cuda.current_stream(dev)
+        self.stages = [("bwd_prepare", L.BWD_PREPARE), ("bwd_dkdv", L.BWD_DKDV), ("bwd_dq", L.BWD_DQ),
+                       ("bwd_finish", L.BWD_FINISH)]
+        self.names = ["reconstruct_kv", "attn_fwd"] + [n for n, _ in self.stages]
+
+    def step(self, ev=None, on=None):
+        L, d, p = self.L, self.d, self.p
+        s = self.stream if on is None else on
         if ev: ev[0].record(s)
-        L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"], kv=kv, stream=s)
+        if not self.fused:
+            L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"], kv=self.kv, stream=s)
         if ev: ev[1].record(s)
-        L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv, out=out, lse=lse,
-                        workspace=ws_f, stream=s)
+        L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=self.kv, out=self.out, lse=self.lse,
+                        workspace=self.ws_f, stream=s)
         if ev: ev[2].record(s)
-        for i, (_, st) in enumerate(stages):
-            L.laga_attn_bwd_stage(st, p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"],
-                                  dq, dc, dkpe, dw, ws_b, stream=s)
+        for i, (_, st) in enumerate(self.stages):
+            L.laga_attn_bwd_stage(st, p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], self.kv, self.out, self.lse,
+                                  d["dout"], self.dq, self.dc, self.dkpe, self.dw, self.ws_b, stream=s)
             if ev: ev[3 + i].record(s)
 
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
-    t0 = time.perf_counter()
-    for i in range(steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    parts = {n: [] for n in names + ["attn_bwd", "step"]}
-    for e in evs:
-        for i, n in enumerate(names):
-            parts[n].append(e[i].elapsed_time(e[i + 1]))
-        parts["attn_bwd"].append(e[2].elapsed_time(e[len(names)]))
-        parts["step"].append(e[0].elapsed_time(e[len(names)]))
-    def median(v):
-        v = sorted(v)
-        return v[len(v) // 2] if len(v) % 2 else 0.5 * (v[len(v) // 2 - 1] + v[len(v) // 2])
-    # per-part medians over the timed steps (the step total is the median of the totals)
-    res = {"wall_ms_per_step": 1e3 * wall / steps,
-           "ms": {k: median(v) for k, v in parts.items()},
-           "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
-    assert torch.isfinite(out).all() and torch.isfinite(dq).all() and torch.isfinite(dw).all()
+    def time(self, steps, warmup):
+        """Median (and min / max) ms of the step and of each entry point over `steps` steps."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(self.names) + 1)] for _ in range(steps)]
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(evs[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        parts = {n: [] for n in self.names + ["attn_bwd", "step"]}
+        for e in evs:
+            for i, n in enumerate(self.names):
+                parts[n].append(e[i].elapsed_time(e[i + 1]))
+            parts["attn_bwd"].append(e[2].elapsed_time(e[len(self.names)]))
+            parts["step"].append(e[0].elapsed_time(e[len(self.names)]))
+        assert torch.isfinite(self.out).all() and torch.isfinite(self.dq).all() and torch.isfinite(self.dw).all()
+        return {"wall_ms_per_step": 1e3 * wall / steps, "ms": {k: _median(v) for k, v in parts.items()},
+                "ms_min_step": min(parts["step"]), "ms_max_step": max(parts["step"])}
 
-    res["graph_ms_per_step"] = graph_step_ms(step, steps) if graph else None
-    res["prologue"] = prologue_bench(w, p, steps, warmup)
+
+def gpu_bench(w, steps, warmup, clock_probe_s=0.0, graph=False, extras=True):
+    import torch
+    import paper_2607_17644_amd as L
+
+    main = StepRunner(w)
+    res = main.time(steps, warmup)
+    res["graph_ms_per_step"] = graph_step_ms(main.step, steps) if graph else None
+    res["workspace_bytes"] = main.ws_bytes
+    if not extras:
+        return res
+    res["prologue"] = prologue_bench(w, main.p, steps, warmup)
     if clock_probe_s > 0:
-        res["clock"] = clock_under_load(step, clock_probe_s)
+        res["clock"] = clock_under_load(main.step, clock_probe_s)
+    out_m, lse_m = main.out.clone(), main.lse.clone()
+    dq_m = main.dq.clone()
+    grads_m = [t.clone() for t in (main.dc, main.dkpe, main.dw)]
+    del main
+    torch.cuda.empty_cache()
 
-    if fused_compare:
-        pf = L.Problem(**{**p.__dict__, "kv_mode": L.KV_FUSED})
-        ws_ff = torch.empty(max(1, L.laga_workspace_bytes(pf, L.OP_FWD)), dtype=torch.uint8, device=dev)
-        out_f = torch.empty_like(out); lse_f = torch.empty_like(lse)
-        fe = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        try:
-            for i in range(warmup + steps):
-                if i == warmup: fe[0].record(stream)
-                L.laga_attn_fwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], out=out_f, lse=lse_f,
-                                workspace=ws_ff, stream=stream)
-            fe[1].record(stream)
-            torch.cuda.synchronize()
-            res["fused_fwd_ms"] = fe[0].elapsed_time(fe[1]) / steps
-            res["fused_vs_materialised_max_abs"] = float((out_f.float() - out.float()).abs().max())
-        except L.LagaError as e:
-            res["fused_fwd_ms"] = None
-            res["fused_error"] = str(e)
+    # the same step without any S x S buffer (dq recomputed)
+    rec = StepRunner(w, dq_mode=L.DQ_RECOMPUTE)
+    r = rec.time(steps, warmup)
+    res["dq_recompute"] = {"ms_per_step": r["ms"]["step"], "ms_breakdown": r["ms"],
+                           "workspace_bytes": rec.ws_bytes,
+                           "dq_max_abs_vs_store": float((rec.dq.float() - dq_m.float()).abs().max()),
+                           "other_grads_bitwise_equal": all(torch.equal(a, b) for a, b in
+                                                            zip((rec.dc, rec.dkpe, rec.dw), grads_m))}
+    del rec
+    torch.cuda.empty_cache()
+
+    # K/V rebuilt on chip from the latent (kv_mode FUSED): forward and whole step
+    fu = StepRunner(w, kv_mode=L.KV_FUSED)
+    r = fu.time(steps, warmup)
+    res["fused"] = {"ms_per_step": r["ms"]["step"], "ms_breakdown": r["ms"], "workspace_bytes": fu.ws_bytes,
+                    "fwd_out_lse_bitwise_equal_materialised": bool(torch.equal(fu.out, out_m) and
+                                                                   torch.equal(fu.lse, lse_m)),
+                    "grads_bitwise_equal_materialised": bool(torch.equal(fu.dq, dq_m) and all(
+                        torch.equal(a, b) for a, b in zip((fu.dc, fu.dkpe, fu.dw), grads_m)))}
+    del fu
+    torch.cuda.empty_cache()
     return res
+
+
+def sweep_bench(w, lengths, steps, warmup):
+    """The default step at shorter gathered sequences (same heads and widths)."""
+    import torch
+    out = []
+    for S in lengths:
+        ws = w.replace(seq_len=S)
+        r = StepRunner(ws).time(steps, warmup)
+        ms = r["ms"]["step"]
+        tf = flops(ws) / (ms * 1e-3) / 1e12
+        out.append({"seq_len": S, "ms_per_step": round(ms, 4), "tflops": round(tf, 1),
+                    "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+                    "ms_breakdown": {k: round(v, 4) for k, v in r["ms"].items()}})
+        torch.cuda.empty_cache()
+    return out
+
+
+def fused_fwd_flops(w, br=256, bc=64):
+    """Executed MFMA flops of the fused forward: the attention (causal, S^2/2 convention) plus
+    the K/V rebuild that every (query block of br rows, key tile of bc keys) pair repeats."""
+    S, H = w.seq_len, w.n_heads
+    nq = (S + br - 1) // br
+    tiles = sum(((qb + 1) * br + bc - 1) // bc for qb in range(nq))
+    rebuild = tiles * 2.0 * bc * w.d_c * w.d_kvh * H * w.batch
+    return float(w.batch) * S * S * H * (w.d_qk + w.d_v) + rebuild
 
 
 def graph_step_ms(step, steps):
@@ -401,7 +459,8 @@ def prologue_bench(w, p, steps, warmup):
 
 
 def cpu_baseline(w, heads):
-    """The oracle as it stands (numpy fp64), on `heads` heads of the same workload."""
+    """The oracle as it stands (numpy), forward + backward on `heads` heads of the same
+    workload: fp32 (the timed baseline) and fp64 (the precision the parity tests use)."""
     import numpy as np
     import laga_inputs as LI
     from oracle import laga as O
@@ -411,17 +470,20 @@ def cpu_baseline(w, heads):
     except Exception:
         threads = os.cpu_count()
     ws = w.replace(n_heads=heads)
-    x = {k: v.astype(np.float64) for k, v in LI.make_inputs(ws).items()}
+    x = LI.make_inputs(ws)
     kw = dict(n_heads=heads, d_nope=ws.d_nope, d_v=ws.d_v, scale=ws.scale)
-    t0 = time.perf_counter()
-    O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **kw)
-    O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **kw)
-    dt = time.perf_counter() - t0
     f = step_flops(ws.batch, ws.seq_len, heads, ws.d_c, ws.d_qk, ws.d_v, ws.d_kvh)
-    return {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"oracle fp64 numpy fwd+bwd (bwd recomputes the forward) of {heads} of {w.n_heads} "
-                      f"heads at S={w.seq_len}: {f / 1e9:.1f} GFLOP in {dt:.1f} s",
-            "seconds": dt}
+    secs = {}
+    for name, dt in (("fp32", np.float32), ("fp64", np.float64)):
+        xs = {k: v.astype(dt) for k, v in x.items()}
+        t0 = time.perf_counter()
+        O.attn_fwd(xs["q"], xs["c_kv"], xs["k_pe"], xs["w_kv_b"], dtype=dt, **kw)
+        O.attn_bwd(xs["q"], xs["c_kv"], xs["k_pe"], xs["w_kv_b"], xs["dout"], dtype=dt, **kw)
+        secs[name] = time.perf_counter() - t0
+    return {"value": f / secs["fp32"] / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"oracle numpy fp32 fwd+bwd (the bwd recomputes the forward) of {heads} of {w.n_heads} "
+                      f"heads at S={w.seq_len}: {f / 1e9:.1f} GFLOP in {secs['fp32']:.1f} s",
+            "seconds": secs["fp32"], "fp64_value": f / secs["fp64"] / 1e12, "fp64_seconds": secs["fp64"]}
 
 
 def main():
@@ -444,7 +506,7 @@ def main():
         pmc_probe(w)
         return
     fl = flops(w)
-    g = gpu_bench(w, a.steps, a.warmup, a.fused_compare, a.clock_probe, graph=not a.no_graph)
+    g = gpu_bench(w, a.steps, a.warmup, a.clock_probe, graph=not a.no_graph, extras=not a.no_extras)
     ms = g["ms"]["step"]
     tflops = fl / (ms * 1e-3) / 1e12
 
@@ -468,8 +530,9 @@ def main():
     cpu = None
     if not a.no_cpu_baseline:
         cpu = cpu_baseline(w, a.cpu_heads)
+    rd = lambda dct: {k: round(v, 4) for k, v in dct.items()}
     line = {
-        "metric": "attention-block TFLOP/s and ms/step (fwd+bwd), S=16384, 16 heads, % bf16 MFMA peak",
+        "metric": f"attention-block TFLOP/s and ms/step (fwd+bwd), S={S}, {H} heads, % bf16 MFMA peak",
         "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": round(ms, 4), "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "graph_ms_per_step": None if g["graph_ms_per_step"] is None else round(g["graph_ms_per_step"], 4),
@@ -478,22 +541,41 @@ def main():
         "config": {"workload": w.name + (f"@S={w.seq_len}" if a.seq_len else "") + (f"@H={H}" if a.heads else ""),
                    "seq_len": S,
                    "n_heads": H, "d_c": w.d_c, "d_nope": w.d_nope, "d_rope": w.d_rope, "d_v": w.d_v,
-                   "batch": w.batch, "causal": True, "kv_mode": "materialised", "deterministic": True,
-                   "algorithmic_gflop_per_step": round(fl / 1e9, 1)},
-        "ms_breakdown": {k: round(v, 4) for k, v in g["ms"].items()},
+                   "batch": w.batch, "causal": True, "kv_mode": "materialised", "dq_mode": "from_store",
+                   "deterministic": True, "algorithmic_gflop_per_step": round(fl / 1e9, 1),
+                   "workspace_bytes": g["workspace_bytes"]},
+        "ms_breakdown": rd(g["ms"]),
         "ms_min_max_step": [round(g["ms_min_step"], 4), round(g["ms_max_step"], 4)],
         "roofline": roofline,
         "algorithmic_tflops_by_kernel": other,
-        "prologue_outside_step": g.get("prologue"),
-        "clock_under_load": g.get("clock"),
-        "cpu_baseline": cpu,
     }
-    if a.fused_compare:
-        line["fused_fwd_ms"] = g.get("fused_fwd_ms")
-        if "fused_error" in g:
-            line["fused_error"] = g["fused_error"]
-        if "fused_vs_materialised_max_abs" in g:
-            line["fused_vs_materialised_max_abs"] = g["fused_vs_materialised_max_abs"]
+    if "dq_recompute" in g:
+        r = g["dq_recompute"]
+        line["dq_recompute"] = {"ms_per_step": round(r["ms_per_step"], 4),
+                                "tflops": round(fl / (r["ms_per_step"] * 1e-3) / 1e12, 1),
+                                "ms_breakdown": rd(r["ms_breakdown"]), "workspace_bytes": r["workspace_bytes"],
+                                "dq_max_abs_vs_store": r["dq_max_abs_vs_store"],
+                                "other_grads_bitwise_equal": r["other_grads_bitwise_equal"]}
+    if "fused" in g:
+        r = g["fused"]
+        fwd_ms = r["ms_breakdown"]["attn_fwd"]
+        ex = fused_fwd_flops(w)
+        line["fused"] = {"ms_per_step": round(r["ms_per_step"], 4),
+                         "tflops_algorithmic": round(fl / (r["ms_per_step"] * 1e-3) / 1e12, 1),
+                         "fwd_ms": round(fwd_ms, 4), "materialised_fwd_plus_reconstruct_ms":
+                             round(g["ms"]["attn_fwd"] + g["ms"]["reconstruct_kv"], 4),
+                         "fwd_tflops_algorithmic": round((fwd_flops + 2.0 * w.batch * S * w.d_c * H * w.d_kvh)
+                                                         / (fwd_ms * 1e-3) / 1e12, 1),
+                         "fwd_tflops_executed": round(ex / (fwd_ms * 1e-3) / 1e12, 1),
+                         "fwd_executed_gflop": round(ex / 1e9, 1),
+                         "ms_breakdown": rd(r["ms_breakdown"]), "workspace_bytes": r["workspace_bytes"],
+                         "fwd_out_lse_bitwise_equal_materialised": r["fwd_out_lse_bitwise_equal_materialised"],
+                         "grads_bitwise_equal_materialised": r["grads_bitwise_equal_materialised"]}
+    if not a.no_extras and a.seq_len is None:
+        line["sweep"] = sweep_bench(w, (2048, 4096, 8192), a.steps, a.warmup)
+    line["prologue_outside_step"] = g.get("prologue")
+    line["clock_under_load"] = g.get("clock")
+    line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
 
 

@@ -54,11 +54,11 @@
  *     W = d_nope + max(d_rope, d_v) + max(d_nope, d_v), B*S*d_c, B*S, and
  *     16*d_c*H*(d_nope + d_v) must each stay below 2^31, else
  *     LAGA_ERR_UNSUPPORTED (and laga_workspace_bytes() returns 0). Memory,
- *     not this limit, bounds S first for the backward: its dS^T store holds
- *     B*H*S*S/2 bf16 values.
+ *     not this limit, bounds S first for the backward with dq_mode FROM_STORE:
+ *     its dS^T store holds B*H*S*S/2 bf16 values (dq_mode RECOMPUTE has none).
  *   - Results do not depend on H: every per-head output (kv columns, out, lse,
  *     dq, dw_kv_b columns) of a head is bit-identical whichever head shard it is
- *     computed in; with deterministic = 1 repeated calls are bit-identical.
+ *     computed in; repeated calls are bit-identical.
  */
 #ifndef LAGA_H_
 #define LAGA_H_
@@ -76,7 +76,7 @@
 extern "C" {
 #endif
 
-#define LAGA_ABI_VERSION 2
+#define LAGA_ABI_VERSION 3
 
 typedef enum {
   LAGA_OK = 0,
@@ -98,6 +98,18 @@ typedef enum { LAGA_KV_MATERIALIZED = 0, LAGA_KV_FUSED = 1 } laga_kv_mode_t;
 
 typedef enum { LAGA_OP_FWD = 0, LAGA_OP_BWD = 1, LAGA_OP_PROLOGUE_BWD = 2 } laga_op_t;
 
+/* How the backward gets dq = scale * dZ K (dZ = P * (dP - delta), the score gradient).
+ * FROM_STORE: the key-stationary pass that forms dZ for dK also writes it (bf16) to a
+ *        store in the workspace, and the dq pass is a product over that store. This
+ *        is the fastest path, but the store holds B*H*S*S/2 values (about 4.3 GB at
+ *        S = 16384, H = 16). Only bf16 with 192/128-wide heads has it; other problems
+ *        recompute (below) whatever this field says.
+ * RECOMPUTE: no buffer of S*S size anywhere (workspace linear in S): the dq pass is
+ *        query-stationary and recomputes the scores and dP for its queries, which costs
+ *        the Q K^T and dO V^T products a second time. Results equal FROM_STORE's up to
+ *        fp32 summation order (dq) or exactly (every other output). */
+typedef enum { LAGA_DQ_FROM_STORE = 0, LAGA_DQ_RECOMPUTE = 1 } laga_dq_mode_t;
+
 typedef struct {
   int64_t batch;       /* B */
   int64_t seq_len;     /* S: gathered sequence length */
@@ -110,8 +122,10 @@ typedef struct {
   int32_t causal;      /* 1: causal mask, 0: none */
   int32_t dtype;       /* laga_dtype_t: element type of all non-fp32 tensors */
   int32_t kv_mode;     /* laga_kv_mode_t */
-  int32_t deterministic; /* 1: no floating-point atomics; bitwise-reproducible */
-  int32_t reserved;    /* must be 0 */
+  int32_t deterministic; /* 1: asks for bitwise-reproducible results. Every kernel of
+                            this library is deterministic (no floating-point atomics),
+                            so 0 is accepted and changes nothing */
+  int32_t dq_mode;     /* laga_dq_mode_t */
 } laga_problem_t;
 
 /* Alg. 1 step 4: kv[b,t,:] = c_kv[b,t,:] @ w_kv_b, stored [B,S,H,d_nope+d_v].
@@ -150,11 +164,11 @@ LAGA_API laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q,
  *   LAGA_BWD_PREPARE  per-row delta = sum(dout * out) (and the K/V rebuild of
  *                     the FUSED mode when kv is NULL)
  *   LAGA_BWD_DKDV     key-stationary attention backward: dK, dV of every key
- *                     (bf16 with 192/128-wide heads: also stores dS^T of every
- *                     causal pair, bf16, in the workspace)
- *   LAGA_BWD_DQ       attention backward for dq (bf16 with 192/128-wide heads:
- *                     the product K^T dS^T over the stored dS^T; otherwise a
- *                     query-stationary pass that recomputes the scores)
+ *                     (bf16 with 192/128-wide heads and dq_mode FROM_STORE: also
+ *                     stores dS^T of every causal pair, bf16, in the workspace)
+ *   LAGA_BWD_DQ       attention backward for dq (with the store: the product
+ *                     K^T dS^T over it; otherwise a query-stationary pass that
+ *                     recomputes the scores)
  *   LAGA_BWD_FINISH   dk_pe head sum, dc_kv and dw_kv_b up-projection GEMMs
  * Each stage reads what the previous ones left in the workspace. */
 typedef enum {
@@ -225,9 +239,10 @@ LAGA_API laga_status_t laga_prologue_bwd(const laga_problem_t* p, const laga_pro
 
 /* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
  * is invalid (check with the entry point itself for the error code). For the
- * backward in bf16 with 192/128-wide heads this includes the dS^T store:
- * 2 * B * H * 512 * T * (T + 1) bytes with the causal mask (2 * B * H * 1024 * T^2
- * without), T = ceil(S / 32) -- about 4.3 GB at S = 16384, H = 16. */
+ * backward in bf16 with 192/128-wide heads and dq_mode FROM_STORE this includes the
+ * dS^T store: 2 * B * H * 512 * T * (T + 1) bytes with the causal mask
+ * (2 * B * H * 1024 * T^2 without), T = ceil(S / 32) -- about 4.3 GB at S = 16384,
+ * H = 16. With dq_mode RECOMPUTE the backward workspace is linear in S. */
 LAGA_API size_t laga_workspace_bytes(const laga_problem_t* p, int op);
 
 /* Static, never-NULL description of a status code. */

@@ -9,7 +9,6 @@ from __future__ import annotations
 
 import ctypes
 import dataclasses
-import math
 import os
 
 import torch
@@ -18,6 +17,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_PKG, "liblaga.so")
 
 DTYPE_BF16, DTYPE_FP32 = 0, 1
+DQ_FROM_STORE, DQ_RECOMPUTE = 0, 1
 KV_MATERIALIZED, KV_FUSED = 0, 1
 OP_FWD, OP_BWD, OP_PROLOGUE_BWD = 0, 1, 2
 BWD_PREPARE, BWD_DKDV, BWD_DQ, BWD_FINISH = 0, 1, 2, 3
@@ -37,7 +37,7 @@ class _CProblem(ctypes.Structure):
                 ("d_c", ctypes.c_int64), ("d_nope", ctypes.c_int64), ("d_rope", ctypes.c_int64),
                 ("d_v", ctypes.c_int64), ("softmax_scale", ctypes.c_float), ("causal", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("kv_mode", ctypes.c_int32), ("deterministic", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("dq_mode", ctypes.c_int32)]
 
 
 class _CPrologue(ctypes.Structure):
@@ -54,20 +54,17 @@ class Problem:
     d_nope: int
     d_rope: int
     d_v: int
-    softmax_scale: float | None = None  # default 1/sqrt(d_nope + d_rope)
+    softmax_scale: float  # multiplies q.k; the caller chooses it (the library has no default)
     causal: int = 1
     dtype: int = DTYPE_BF16
     kv_mode: int = KV_MATERIALIZED
     deterministic: int = 1
-    reserved: int = 0
+    dq_mode: int = DQ_FROM_STORE
 
     def c(self) -> _CProblem:
-        scale = self.softmax_scale
-        if scale is None:
-            scale = 1.0 / math.sqrt(self.d_nope + self.d_rope)
         return _CProblem(self.batch, self.seq_len, self.n_heads, self.d_c, self.d_nope, self.d_rope,
-                         self.d_v, scale, self.causal, self.dtype, self.kv_mode, self.deterministic,
-                         self.reserved)
+                         self.d_v, self.softmax_scale, self.causal, self.dtype, self.kv_mode,
+                         self.deterministic, self.dq_mode)
 
     @property
     def torch_dtype(self):

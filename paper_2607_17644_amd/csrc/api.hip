@@ -29,7 +29,7 @@ laga_status_t validate(const laga_problem_t* p, Dims* d) {
     return LAGA_ERR_SHAPE;
   if (!isfinite(p->softmax_scale) || !(p->softmax_scale > 0.f)) return LAGA_ERR_SHAPE;
   if ((p->causal != 0 && p->causal != 1) || (p->deterministic != 0 && p->deterministic != 1) ||
-      p->reserved != 0)
+      (p->dq_mode != LAGA_DQ_FROM_STORE && p->dq_mode != LAGA_DQ_RECOMPUTE))
     return LAGA_ERR_UNSUPPORTED;
   if (p->dtype != LAGA_DTYPE_BF16 && p->dtype != LAGA_DTYPE_FP32) return LAGA_ERR_UNSUPPORTED;
   if (p->kv_mode != LAGA_KV_MATERIALIZED && p->kv_mode != LAGA_KV_FUSED) return LAGA_ERR_UNSUPPORTED;
@@ -53,11 +53,19 @@ size_t elem_size(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 ?
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Backward workspace: [delta | lse2 | dKV | dKV low halves (bf16) | dK_pe per head | GEMM split partials |
-// kv rebuild | dS^T store (bf16 with 192/128-wide heads)]
+// fused mode: W_kv_b^T (K/V rebuilt on chip) or the kv rebuild | dS^T store (bf16 with 192/128-wide heads)]
 struct BwdWs {
-  size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, ds, total;
+  size_t delta, lse2, dkv, dkv_lo, dkpe_h, dw_part, kv, w_t, ds, total;
 };
-bool stores_ds(const laga_problem_t* p) { return p->dtype == LAGA_DTYPE_BF16 && is_v3(p); }
+bool stores_ds(const laga_problem_t* p) {
+  return p->dtype == LAGA_DTYPE_BF16 && is_v3(p) && p->dq_mode == LAGA_DQ_FROM_STORE;
+}
+// Fused mode without kv: the key-stationary and dQ kernels rebuild K/V tiles on chip from
+// c_kv and W_kv_b^T (bf16 with 192/128-wide heads, dq from the store); other problems
+// rebuild kv once into the workspace and run the materialised kernels.
+bool kv_on_chip(const laga_problem_t* p) {
+  return p->kv_mode == LAGA_KV_FUSED && stores_ds(p) && p->d_c <= kFusedMaxDc;
+}
 int s_pad(int S) { return (S + kRowPad - 1) / kRowPad * kRowPad; }
 BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   BwdWs w{};
@@ -70,7 +78,9 @@ BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
   w.dkpe_h = off; off += round_up(sizeof(float) * tok * d.H * d.dr);
   const size_t np = gemm_partial_elems((int)tok, d.d_c, d.H * d.dkvh());
   w.dw_part = off; off += np > 0 ? round_up(sizeof(float) * np) : 0;
-  w.kv = off; off += p->kv_mode == LAGA_KV_FUSED ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
+  const bool fused = p->kv_mode == LAGA_KV_FUSED;
+  w.kv = off; off += fused && !kv_on_chip(p) ? round_up(elem_size(p) * tok * d.H * d.dkvh()) : 0;
+  w.w_t = off; off += kv_on_chip(p) ? round_up(elem_size(p) * (size_t)d.d_c * d.H * d.dkvh()) : 0;
   w.ds = off;
   off += stores_ds(p) ? round_up(sizeof(uint16_t) * (size_t)d.B * d.H * bwd::ds_head_elems((d.S + 31) / 32, p->causal)) : 0;
   w.total = off;
@@ -256,7 +266,14 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
   const bool bf = p->dtype == LAGA_DTYPE_BF16;
   const bool v3 = is_v3(p);
 
-  if (fused && !kv) {
+  const bool on_chip = fused && !kv && kv_on_chip(p);
+  if (on_chip) {
+    // the kernels rebuild K/V tiles from c_kv and W_kv_b^T, transposed in the first stage
+    if (stage == LAGA_BWD_PREPARE) {
+      hipError_t e = launch_transpose_w<bf16>((const bf16*)w_kv_b, (bf16*)(wsb + ws.w_t), d.d_c, d.H * d.dkvh(), st);
+      if (e != hipSuccess) return LAGA_ERR_DEVICE;
+    }
+  } else if (fused && !kv) {
     // K/V are rebuilt (same GEMM as laga_reconstruct_kv) into the workspace in the first stage.
     void* kvw = wsb + ws.kv;
     if (stage == LAGA_BWD_PREPARE) {
@@ -266,6 +283,8 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
     kv = kvw;
   }
   AttnBwdArgs a{};
+  a.c_kv = c_kv; a.d_c = d.d_c;
+  a.w_t = on_chip ? wsb + ws.w_t : nullptr;
   a.q = q; a.k_pe = k_pe; a.kv = kv; a.out = out; a.dout = dout; a.lse = lse; a.dq = dq;
   a.delta = (float*)(wsb + ws.delta); a.dkv = wsb + ws.dkv; a.dkpe_h = (float*)(wsb + ws.dkpe_h);
   a.lse2 = (float*)(wsb + ws.lse2); a.S_pad = s_pad(d.S);

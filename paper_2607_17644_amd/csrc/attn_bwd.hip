@@ -21,8 +21,8 @@
 //                  transposing LDS reads; it recomputes S and dP (the price of
 //                  not accumulating dQ with atomics)
 //   dkdv32_kernel  the same for bf16 with 192/128-wide heads, 32 keys per wave on
-//                  the 32x32x16 MFMA, software-pipelined (see there); it also
-//                  stores dS^T for the dQ pass
+//                  the 32x32x16 MFMA, software-pipelined (see there); unless dq is
+//                  to be recomputed, it also stores dS^T for the dQ pass
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
 #include <type_traits>
 
@@ -288,6 +288,12 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 //   A(t): S = Q K^T, dP = dO V^T        20 MFMAs on Q / dO row fragments
 //   B(t): P = exp2(S c - lse2), dZ = P (dP - delta), the dS^T store    VALU
 //   C(t): dV^T += dO^T P, dK^T += Q^T dZ  20 MFMAs on transposing reads of dO / Q
+// In the first key block of each head (keys 0..127) the rope band of dK^T also takes dZ's
+// low part (dZ as a bf16 pair hi + lo, 4 more MFMAs per tile): dk_pe sums that band over
+// every head, and the first keys are the ones every query attends to, so there the bf16
+// rounding of dZ, summed over all queries, is the largest error of the block's gradients;
+// a key j's share of it scales with sum_i P_ij^2, which falls off quickly past the first
+// keys. dK_nope, dV and dQ take the hi part only.
 // With no second wave on its SIMD to hide latencies, the wave overlaps B(t-1) with A(t)
 // (the softmax of one tile beside the MFMAs of the next; S and dP of consecutive tiles
 // alternate between two accumulator sets), then runs C(t-1); the instruction order is
@@ -300,7 +306,18 @@ __global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
 // the four slots and every LDS read is a per-lane base register plus an immediate
 // offset, with no address arithmetic in the loop. The per-wave issue rate, not the LDS,
 // is then its limit. It also stores dZ (bf16) as dS^T for the dQ pass.
-template <int DN, int DR, int DV>
+// Low part of an accumulator half rounded to bf16: bf16(x - float(hi)) for the 8 values
+// that acc_to_frag turned into `hi`, so that hi + lo carries about 16 significant bits
+// (x - float(hi) is exact in fp32).
+__device__ __forceinline__ bf16x8 acc_lo_frag(const f32x16& acc, int half, const bf16x8& hi) {
+  typedef float f32x8v __attribute__((ext_vector_type(8)));
+  f32x8v v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = acc[8 * half + e] - (float)hi[e];
+  return __builtin_convertvector(v, bf16x8);
+}
+
+template <int DN, int DR, int DV, bool STORE_DS, bool FUSED>
 __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, NW = 4, BK = 32 * NW, BQ = 32, NS = 4;
@@ -311,6 +328,10 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   static_assert(KQ * 64 * NW == QCH && KO * 64 * NW == OCH && 5 * (KQ + KO) <= 32, "load split");
   constexpr int F = KQ + KO + 1;
   constexpr int QTB = QCH * 16, OTB = OCH * 16;  // tile bytes
+  // dK^T blocks RB, RB + 1 are the rope band [DN, DN + DR): their product takes dZ as a bf16
+  // pair hi + lo, because dk_pe sums that band over every head and every query
+  constexpr int RB = DN / 32;
+  static_assert(DR == 64 && RB + 2 == DQK / 32, "two 32-wide rope blocks at the end of dK^T");
   __shared__ __attribute__((aligned(16))) T sQ[NS][QCH * 8];
   __shared__ __attribute__((aligned(16))) T sO[NS][OCH * 8];
   __shared__ __attribute__((aligned(16))) float sL[NS][NW][256];
@@ -379,7 +400,44 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   };
 
   frag_t<T> kf[DQK / 16], vf[DV / 16];
-  {
+  if constexpr (FUSED) {
+    // The wave's K_nope / V rows rebuilt from the latent: KV^T (kv columns x 32 keys) =
+    // W_h^T c^T, contracted over d_c in ascending 16-wide steps from zero with A = rows of
+    // W^T and B = rows of c - the operand roles, order and bf16 rounding of the up-
+    // projection GEMM, so every element equals the materialised kv bit for bit. The
+    // accumulator lays lane (n, g) on rows 8 (r / 4) + 4 g + r % 4 of a 32-column block;
+    // feeding W^T's rows in the order pi (bits 2 and 3 of the row swapped) puts columns
+    // 16 h + 8 g + e (h = r / 8, e = r % 8) there instead, which is exactly the layout of
+    // the two 16-wide B-operand fragments of that block: no data movement afterwards.
+    static_assert(DN % 32 == 0 && DV % 32 == 0, "32-column blocks");
+    const int dc = P.d_c;
+    const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
+    const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + pi_n) * dc + 8 * g;
+    const T* cr = (const T*)P.c_kv + krow * dc + 8 * g;
+    constexpr int NB = DKVH / 32;
+    f32x16 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = f32x16{};
+    for (int ks = 0; ks < dc / 16; ++ks) {
+      const frag_t<T> cf = *reinterpret_cast<const frag_t<T>*>(cr + ks * 16);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        mma(acc[b], *reinterpret_cast<const frag_t<T>*>(wt + (size_t)b * 32 * dc + ks * 16), cf);
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const frag_t<T> f = key_ok ? acc_to_frag<T>(acc[b], hh) : frag_t<T>{};
+        if (b < DN / 32) kf[2 * b + hh] = f;
+        else vf[2 * (b - DN / 32) + hh] = f;
+      }
+#pragma unroll
+    for (int ks = DN / 16; ks < DQK / 16; ++ks) {
+      kf[ks] = *reinterpret_cast<const frag_t<T>*>(kpe + krow * DR + (ks - DN / 16) * 16 + 8 * g);
+      if (!key_ok) kf[ks] = frag_t<T>{};
+    }
+  } else {
     const T* kvr = kv + (krow * H + h) * DKVH;
 #pragma unroll
     for (int ks = 0; ks < DQK / 16; ++ks) {
@@ -465,7 +523,9 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
         sa[r] = (unsigned)(qt + (r >> 2) * 8 + g * 4 + (r & 3) - q_lo) < q_span ? sa[r] : -INFINITY;
     }
   };
-  auto step_b = [&](int st, const f32x16& sa, const f32x16& dp, bf16x8 (&pf)[2], bf16x8 (&zf)[2]) {
+  auto step_b = [&](auto hc, int st, const f32x16& sa, const f32x16& dp, bf16x8 (&pf)[2], bf16x8 (&zf)[2],
+                    bf16x8 (&zl)[2]) {
+    constexpr bool HILO = decltype(hc)::value;
     const float* tl = sL[st][wave];
     f32x16 p, z;
 #pragma unroll
@@ -482,10 +542,12 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     for (int kk = 0; kk < BQ / 16; ++kk) {
       pf[kk] = acc_to_frag<T>(p, kk);
       zf[kk] = acc_to_frag<T>(z, kk);
+      if constexpr (HILO) zl[kk] = acc_lo_frag(z, kk, zf[kk]);
     }
   };
-  T* const dsw = (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, 0) + (size_t)k0 * BQ;
+  T* const dsw = STORE_DS ? (T*)P.ds + ds_tile_offset(P.ds_T, P.causal, bh, 0) + (size_t)k0 * BQ : nullptr;
   auto store_ds = [&](int j, const bf16x8 (&zf)[2]) {
+    if constexpr (!STORE_DS) return;
     const int t = (qt_begin + j * BQ) / BQ;
     if (my_k < ds_tile_keys(P.ds_T, P.causal, t)) {
       // accumulator element r of this lane is query 8 (r / 4) + 4 g + r % 4: position 16 g + r.
@@ -503,10 +565,14 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     if (j + 2 < ntiles) fill((j + 2) % NS, qt_begin + (j + 2) * BQ);
   };
 
+  // The sweep over the query tiles, compiled twice: with HILO the rope band of dK^T takes
+  // dZ as a bf16 pair hi + lo (the first key block of each head, see above).
+  auto sweep = [&](auto hc) {
+  constexpr bool HILO = decltype(hc)::value;
   fill(0, qt_begin);
   if (ntiles > 1) fill(1, qt_begin + BQ);
   f32x16 sa0, dp0, sa1, dp1;
-  bf16x8 pf[2], zf[2];
+  bf16x8 pf[2], zf[2], zl[2];
   sync(0);
   step_a(0, sa0, dp0);
   constexpr int PF = 3;
@@ -553,8 +619,9 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     for (int kk = 0; kk < BQ / 16; ++kk) {
       pf[kk] = acc_to_frag<T>(p, kk);
       zf[kk] = acc_to_frag<T>(z, kk);
+      if constexpr (HILO) zl[kk] = acc_lo_frag(z, kk, zf[kk]);
     }
-    bf16x8 cb[PF + 1];
+    bf16x8 cb[PF + 1], c_r0, c_r1;
 #pragma unroll
     for (int i = 0; i < PF; ++i) cb[i] = c_read(SP, i);
     __builtin_amdgcn_sched_barrier(0);
@@ -564,6 +631,16 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
       const int kk = i / 10, m = i % 10;
       if (m < DQK / 32) mma(dk[m], cb[i % (PF + 1)], zf[kk]);
       else mma(dv[m - DQK / 32], cb[i % (PF + 1)], pf[kk]);
+      // the rope band of dK (blocks RB, RB + 1) also takes dZ's low part, each one
+      // product later so that no MFMA waits on the one just before it
+      if constexpr (HILO) {
+        if (m == RB) c_r0 = cb[i % (PF + 1)];
+        if (m == RB + 1) {
+          c_r1 = cb[i % (PF + 1)];
+          mma(dk[RB], c_r0, zl[kk]);
+        }
+        if (m == RB + 2) mma(dk[RB + 1], c_r1, zl[kk]);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     store_ds(jj - 1, zf);
@@ -589,19 +666,24 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     const int jl = ntiles - 1, sl = jl % NS;
     if (jl & 1) {
       mask_b(jl, sa1);
-      step_b(sl, sa1, dp1, pf, zf);
+      step_b(hc, sl, sa1, dp1, pf, zf, zl);
     } else {
       mask_b(jl, sa0);
-      step_b(sl, sa0, dp0, pf, zf);
+      step_b(hc, sl, sa0, dp0, pf, zf, zl);
     }
 #pragma unroll
     for (int i = 0; i < 20; ++i) {
       const int kk = i / 10, m = i % 10;
-      if (m < DQK / 32) mma(dk[m], c_read(sl, i), zf[kk]);
-      else mma(dv[m - DQK / 32], c_read(sl, i), pf[kk]);
+      const bf16x8 c = c_read(sl, i);
+      if (m < DQK / 32) mma(dk[m], c, zf[kk]);
+      else mma(dv[m - DQK / 32], c, pf[kk]);
+      if (HILO && m >= RB && m < DQK / 32) mma(dk[m], c, zl[kk]);
     }
     store_ds(jl, zf);
   }
+  };
+  if (kb == 0) sweep(std::true_type{});
+  else sweep(std::false_type{});
 
   if (!key_ok) return;
   const size_t row = krow * H + h;
@@ -665,6 +747,7 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
   P.dq = a.dq; P.dkv = a.dkv; P.dkv_lo = a.dkv_lo; P.dkpe_h = a.dkpe_h;
   P.S = a.S; P.H = a.H; P.scale = a.scale; P.scale_log2 = a.scale * 1.4426950408889634f; P.causal = a.causal;
   P.ds = a.ds; P.ds_T = (a.S + 31) / 32;
+  P.c_kv = a.c_kv; P.w_t = a.w_t; P.d_c = a.d_c;
   if (stage == 0) {
     const int BS = a.B * a.S;
     delta_kernel<T, DV><<<(BS + 3) / 4, 256, 0, st>>>((const T*)a.out, (const T*)a.dout, a.lse, a.delta, a.lse2,
@@ -672,7 +755,14 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
   } else if (stage == 1) {
     if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
       P.n_blocks = (a.S + 127) / 128;
-      dkdv32_kernel<DN, DR, DV><<<dim3(P.n_blocks * a.H, a.B), 256, 0, st>>>(P);
+      const dim3 grid(P.n_blocks * a.H, a.B);
+      if (a.w_t) {
+        if (a.ds) dkdv32_kernel<DN, DR, DV, true, true><<<grid, 256, 0, st>>>(P);
+        else dkdv32_kernel<DN, DR, DV, false, true><<<grid, 256, 0, st>>>(P);
+      } else {
+        if (a.ds) dkdv32_kernel<DN, DR, DV, true, false><<<grid, 256, 0, st>>>(P);
+        else dkdv32_kernel<DN, DR, DV, false, false><<<grid, 256, 0, st>>>(P);
+      }
     } else {
       constexpr int BK = 32 * Tl::WPH_KV;
       P.n_blocks = (a.S + BK - 1) / BK;

@@ -279,6 +279,111 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
     }
 }
 
+// dQ from the stored dS^T with K/V rebuilt on chip (kv_mode FUSED; bf16, 192/128-wide
+// heads): as dq_ds_kernel, but no per-head K exists in HBM, so each step's K tile is built
+// in LDS: the K_nope rows of its 64 keys from the latent (KV^T = W_h^T c^T over d_c in
+// ascending 16-wide steps, the up-projection GEMM's operand roles and rounding, so the
+// tile equals the materialised kv bit for bit, and dq equals dq_ds_kernel's), the k_pe
+// rows loaded as they are. Wave w rebuilds the 32 x 32 block (key half w / 4, K_nope
+// columns 32 (w % 4) ..): every wave does the same 32 MFMAs per step, beside its 24 of
+// the dQ product. The rebuild repeats for every query block of 256 rows (the price of a
+// query-stationary pass: d_c * d_nope / (256 * d_qk) of its product flops, 1.33x).
+template <int DN, int DR, int DV>
+__global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = 8, KB = 64;
+  constexpr int KP = DQK / 8 + 4;  // K tile pitch in 16-byte chunks (% 8 == 4: transposing reads)
+  static_assert(DN == 4 * 32 && DR == 64, "four 32-column K_nope blocks, 64-wide k_pe");
+  __shared__ __attribute__((aligned(16))) T sK[KB * KP * 8];
+  __shared__ __attribute__((aligned(16))) T sD[NW * 2 * 32 * 32];
+
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ ds = (const T*)P.ds;
+  const int S = P.S, H = P.H, TT = P.ds_T, dc = P.d_c;
+
+  const int total = P.n_blocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;  // heavy first
+  const int bh = lin / P.n_blocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
+  const int t = qblk * NW + wave;  // this wave's query tile
+  const bool wave_ok = t < TT;
+  const int nk = wave_ok ? ds_tile_keys(TT, P.causal, t) : 0;
+  const T* dtile = ds + (wave_ok ? ds_tile_offset(TT, P.causal, bh, t) : 0);
+  const int kend = P.causal ? min(S, (qblk + 1) * NW * 32) : S;
+  const int nsteps = (kend + KB - 1) / KB;
+
+  // this wave's share of the rebuild: key half rk, K_nope column block rb; W^T rows in the
+  // order pi (bits 2 and 3 swapped) so that lane (n, g) holds columns 16 hh + 8 g + e
+  const int rk = wave >> 2, rb = wave & 3;
+  const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
+  const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + rb * 32 + pi_n) * dc + 8 * g;
+  const T* cg = (const T*)P.c_kv + (size_t)b * S * dc + 8 * g;
+
+  f32x16 dqa[DQK / 32];
+#pragma unroll
+  for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
+
+  for (int st = 0; st < nsteps; ++st) {
+    const int kt = st * KB;
+    __syncthreads();  // the previous step's reads of sK / sD are done
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {  // this wave's dS^T blocks of the step (a dummy when not stored)
+      const int kb = kt + 32 * sub;
+      const T* src = kb < nk ? dtile + (size_t)kb * 32 : dtile;
+      g2lds16(src + l * 8, sD + (wave * 2 + sub) * 1024);
+      g2lds16(src + 512 + l * 8, sD + (wave * 2 + sub) * 1024 + 512);
+    }
+    {  // k_pe rows: wave w copies keys 8 w .. 8 w + 7 (rows past S clamped: their dS is zero)
+      const int r = wave * 8 + (l >> 3);
+      const int key = min(kt + r, S - 1);
+      const chunk16 v = *reinterpret_cast<const chunk16*>(kpe + (size_t)(b * S + key) * DR + (l & 7) * 8);
+      *reinterpret_cast<chunk16*>(sK + r * KP * 8 + DN + (l & 7) * 8) = v;
+    }
+    {  // K_nope block (rk, rb)
+      const int key = min(kt + 32 * rk + n, S - 1);
+      const T* cr = cg + (size_t)key * dc;
+      f32x16 acc = f32x16{};
+      for (int ks = 0; ks < dc / 16; ++ks)
+        mma(acc, *reinterpret_cast<const frag_t<T>*>(wt + ks * 16), *reinterpret_cast<const frag_t<T>*>(cr + ks * 16));
+      T* dst = sK + (32 * rk + n) * KP * 8 + rb * 32 + 8 * g;
+      *reinterpret_cast<bf16x8*>(dst) = acc_to_frag<T>(acc, 0);
+      *reinterpret_cast<bf16x8*>(dst + 16) = acc_to_frag<T>(acc, 1);
+    }
+    wait_vmem();
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      if (kt + 32 * sub < nk) {  // wave-uniform: key blocks past the tile's queries hold no dS
+        const T* tk = sK + 32 * sub * KP * 8;
+        const T* td = sD + (wave * 2 + sub) * 1024;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int ra = kk * 16 + 4 * g;
+          const bf16x8 zf = pad_tr_frag<4>(td, ra, ra + 8, 0);
+#pragma unroll
+          for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], pad_tr_frag<KP>(tk, ra, ra + 8, db * 32), zf);
+        }
+      }
+    }
+  }
+
+  const int my_q = t * 32 + ds_query_of_position(n);
+  if (!wave_ok || my_q >= S) return;
+  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
+#pragma unroll
+  for (int db = 0; db < DQK / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      bf16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
+      *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
+    }
+}
+
 }  // namespace
 
 template <typename T, int DN, int DR, int DV>
@@ -287,12 +392,15 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   constexpr int BR = 32 * Tl::WPH_Q;
   P.n_blocks = (P.S + BR - 1) / BR;
   if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
-    constexpr int WPH = 8;
-    P.n_blocks = (P.ds_T + WPH - 1) / WPH;
-    dq_ds_kernel<DN, DR, DV, WPH, 4><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
-  } else {
-    dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
+    if (P.ds) {
+      constexpr int WPH = 8;
+      P.n_blocks = (P.ds_T + WPH - 1) / WPH;
+      if (P.w_t) dq_ds_fused_kernel<DN, DR, DV><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
+      else dq_ds_kernel<DN, DR, DV, WPH, 4><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
+      return hipGetLastError();
+    }
   }
+  dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
   return hipGetLastError();
 }
 

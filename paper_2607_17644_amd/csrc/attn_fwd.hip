@@ -274,18 +274,22 @@ void attn_fwd_kernel(FwdParams P) {
 // (p = 0, m and O unchanged). Softmax details: the running max is taken on the raw
 // scores (scale > 0), p = exp2(s * scale_log2 - m) is one FMA and one v_exp_f32,
 // and O^T is rescaled only when some lane's running max moved.
-template <int DN, int DR, int DV, int BC, int WPH>
+// G heads per workgroup (WPH / G waves each, 32 * WPH / G queries per head): each key tile
+// stages one K_nope and one V tile per head and ONE k_pe tile that every head's waves read
+// (k_pe is shared by all heads, property P2 of Section 2.1).
+template <int DN, int DR, int DV, int BC, int WPH, int G>
 __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   using T = bf16;
-  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, BR = 32 * WPH;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = WPH, WH = WPH / G, BR = 32 * WH;
   constexpr int KCPR = DN / 8, PCPR = DR / 8, VCPR = DV / 8;
   static_assert(KCPR == 16 && PCPR == 8 && VCPR == 16, "swizzles are defined for 128/64/128-wide rows");
+  static_assert(WPH % G == 0, "whole waves per head");
   // two ring stages as distinct LDS objects: the compiler then sees that the direct
   // loads into one stage cannot alias the reads of the other and does not wait for
   // them (the explicit wait + barrier at the top of each tile orders the stages)
-  __shared__ __attribute__((aligned(16))) T sK0[BC * DN], sK1[BC * DN];
+  __shared__ __attribute__((aligned(16))) T sK0[G * BC * DN], sK1[G * BC * DN];
   __shared__ __attribute__((aligned(16))) T sP0[BC * DR], sP1[BC * DR];
-  __shared__ __attribute__((aligned(16))) T sV0[BC * DV], sV1[BC * DV];
+  __shared__ __attribute__((aligned(16))) T sV0[G * BC * DV], sV1[G * BC * DV];
 
   const T* __restrict__ q = (const T*)P.q;
   const T* __restrict__ kpe = (const T*)P.k_pe;
@@ -295,12 +299,15 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   const int total = P.n_qblocks * P.n_hgroups * gridDim.y;
   const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
   const int qb = P.n_qblocks - 1 - lin % P.n_qblocks;
-  const int bh = lin / P.n_qblocks;
-  const int b = bh / H, h = bh % H;
+  const int bhg = lin / P.n_qblocks;
+  const int b = bhg / P.n_hgroups, h0 = (bhg % P.n_hgroups) * G;
 
   const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int q0 = qb * BR + wave * 32;
+  const int hh = wave / WH;   // this wave's head within the group
+  const int h = min(h0 + hh, H - 1);
+  const bool head_ok = h0 + hh < H;
+  const int q0 = qb * BR + (wave % WH) * 32;
   const int my_q = q0 + n;
   const int kend = P.causal ? min(S, (qb + 1) * BR) : S;
 
@@ -326,9 +333,12 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   vfill.init(wave, l, H * DKVH);
   pfill.init(wave, l, DR);
   auto fill = [&](T* dk, T* dp, T* dv, int kt) {
-    const T* kvb = kv + ((size_t)(b * S + kt) * H + h) * DKVH;
-    kfill.fill(dk, wave, l, kvb, H * DKVH, S - kt);
-    vfill.fill(dv, wave, l, kvb + DN, H * DKVH, S - kt);
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      const T* kvb = kv + ((size_t)(b * S + kt) * H + min(h0 + gi, H - 1)) * DKVH;
+      kfill.fill(dk + gi * BC * DN, wave, l, kvb, H * DKVH, S - kt);
+      vfill.fill(dv + gi * BC * DV, wave, l, kvb + DN, H * DKVH, S - kt);
+    }
     pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, S - kt);
   };
 
@@ -344,9 +354,9 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
       else fill(sK0, sP0, sV0, kt + BC);
     }
     if (P.causal && kt > q0 + 31) return;  // wave-uniform: every key of the tile is masked for this wave
-    const T* tk = ST == 0 ? sK0 : sK1;
+    const T* tk = (ST == 0 ? sK0 : sK1) + hh * BC * DN;
     const T* tp = ST == 0 ? sP0 : sP1;
-    const T* tv = ST == 0 ? sV0 : sV1;
+    const T* tv = (ST == 0 ? sV0 : sV1) + hh * BC * DV;
 
     f32x16 sacc[BC / 32];
 #pragma unroll
@@ -417,7 +427,7 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
 
-  if (my_q >= S) return;
+  if (!head_ok || my_q >= S) return;
   const float ltot = wave_xor32_sum(lsum);
   const float inv = 1.f / ltot;
   T* orow = (T*)P.out + ((size_t)(b * S + my_q) * H + h) * DV;
@@ -648,6 +658,8 @@ template <int DN, int DR, int DV> struct FwdTiles<float, DN, DR, DV> {
 // slower with few heads: its longest workgroup, the first keys', sets the time whatever
 // its width.)
 constexpr int kFwdFillGroups = 512;
+// Heads per workgroup of the bf16 ring forward (one shared k_pe tile per key tile).
+constexpr int kFwdRingHeads = 1;
 
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
@@ -666,9 +678,10 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st) {
     // traffic of 4 waves (measured 8 % faster at S = 16384); 4 waves when 8 would leave
     // fewer than kFwdFillGroups workgroups (few heads or short sequences)
     auto ring = [&](auto rw) {
-      constexpr int RW = decltype(rw)::value, RBR = 32 * RW;
+      constexpr int RW = decltype(rw)::value, RG = kFwdRingHeads, RBR = 32 * RW / RG;
       P.n_qblocks = (a.S + RBR - 1) / RBR;
-      attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, RW><<<dim3(P.n_qblocks * P.n_hgroups, a.B, 1), 64 * RW, 0, st>>>(P);
+      P.n_hgroups = (a.H + RG - 1) / RG;
+      attn_fwd_ring_kernel<DN, DR, DV, Tl::BC, RW, RG><<<dim3(P.n_qblocks * P.n_hgroups, a.B, 1), 64 * RW, 0, st>>>(P);
     };
     if ((long long)((a.S + 255) / 256) * P.n_hgroups * a.B >= kFwdFillGroups) ring(std::integral_constant<int, 8>{});
     else ring(std::integral_constant<int, 4>{});
@@ -699,6 +712,15 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
   attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, FW, kFusedMaxDc><<<grid, 64 * FW, 0, st>>>(P);
   return hipGetLastError();
 }
+
+template <typename T>
+hipError_t launch_transpose_w(const T* w, T* w_t, int K, int N, hipStream_t st) {
+  const long long nw = (long long)K * N;
+  transpose_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>(w, w_t, K, N);
+  return hipGetLastError();
+}
+template hipError_t launch_transpose_w<bf16>(const bf16*, bf16*, int, int, hipStream_t);
+template hipError_t launch_transpose_w<float>(const float*, float*, int, int, hipStream_t);
 
 #define LAGA_INST_FWD(T, DN, DR, DV)                                                      \
   template hipError_t launch_attn_fwd<T, DN, DR, DV>(const AttnFwdArgs&, hipStream_t);    \

@@ -41,6 +41,11 @@ struct BwdParams {
   // pass, read by the dQ pass; see ds_tile_offset. ds_T = ceil(S / 32).
   void* ds;
   int ds_T;
+  // K/V rebuilt on chip (kv_mode FUSED, bf16 with 192/128-wide heads): kv is unused and
+  // each key's K_nope / V rows come from c_kv [B,S,d_c] and w_t = W_kv_b^T [H*(DN+DV), d_c]
+  const void* c_kv;
+  const void* w_t;
+  int d_c;
 };
 
 // dS^T store layout: for every (b, h) and query tile t of 32 rows, the keys that tile

@@ -56,6 +56,9 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
 // Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T
 // (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
 constexpr int kFusedMaxDc = 512;
+// w_t[n][k] = w[k][n] for w [K, N] (W_kv_b^T for the on-chip K/V rebuilds)
+template <typename T>
+hipError_t launch_transpose_w(const T* w, T* w_t, int K, int N, hipStream_t st);
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t st);
 
@@ -75,6 +78,9 @@ struct AttnBwdArgs {
   void* dkv_lo;      // workspace [B,S,H,DN+DV], bf16 only: dKV - bf16(dKV) rounded to bf16
   float* dkpe_h;     // workspace [B,S,H,DR]
   void* ds;          // workspace: dS^T store (bf16 path with 192/128-wide heads), else unused
+  const void* c_kv;  // [B,S,d_c]: with w_t, the latent K/V are rebuilt from (kv unused)
+  const void* w_t;   // W_kv_b^T [H*(DN+DV), d_c] (workspace), or NULL: K/V read from kv
+  int d_c;
   int B, S, H;
   float scale;
   int causal;

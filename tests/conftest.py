@@ -27,3 +27,34 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+@pytest.fixture(autouse=True)
+def sentinel_buffers(request, monkeypatch):
+    """In GPU tests every output and workspace the binding allocates starts as NaN
+    (bytes 0xFF: a NaN in bf16 and in fp32), so an element the library fails to write
+    cannot pass a comparison by holding a previous run's result that the caching
+    allocator handed back."""
+    if "gpu" not in request.keywords:
+        yield
+        return
+    import torch
+    import paper_2607_17644_amd.binding as B
+
+    new0, ws0 = B._new, B._workspace
+
+    def new(p, name, dtype, device):
+        t = new0(p, name, dtype, device)
+        t.view(torch.uint8).fill_(0xFF) if t.numel() else None
+        return t
+
+    def workspace(p, op, ws, device):
+        fresh = ws is None
+        ws = ws0(p, op, ws, device)
+        if fresh:
+            ws.fill_(0xFF)
+        return ws
+
+    monkeypatch.setattr(B, "_new", new)
+    monkeypatch.setattr(B, "_workspace", workspace)
+    yield

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     import paper_2607_17644_amd as L
-    assert L.laga_abi_version() == 2
+    assert L.laga_abi_version() == 3
     for code in range(7):
         assert L.laga_status_string(code).startswith("LAGA_")
     assert "unknown" in L.laga_status_string(99)
@@ -45,7 +45,7 @@ def _raw():
 
 def test_validation_errors_without_launch():
     lib, B = _raw()
-    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128, 0.072)
     fake = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
     vp = ctypes.c_void_p
     # NULL problem
@@ -58,7 +58,7 @@ def test_validation_errors_without_launch():
         assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 2, field
     # unsupported
     for field, val in (("d_nope", 64), ("d_c", 48), ("d_c", 2048), ("dtype", 7), ("kv_mode", 3),
-                       ("causal", 2), ("deterministic", 5), ("reserved", 1)):
+                       ("causal", 2), ("deterministic", 5), ("dq_mode", 2)):
         Q = B.Problem(**{**P.__dict__, field: val})
         assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 3, field
     # 32-bit element offsets: the largest tensor must stay below 2^31 elements
@@ -78,7 +78,7 @@ def test_validation_errors_without_launch():
 
 def test_attention_entry_points_validate_first():
     lib, B = _raw()
-    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128, 0.072)
     fake = ctypes.c_void_p(0x10000)
     z = None
     # materialised forward without kv -> NULL
@@ -99,7 +99,7 @@ def test_attention_entry_points_validate_first():
 
 def test_prologue_entry_points_validate_first():
     lib, B = _raw()
-    P = B.Problem(1, 64, 2, 512, 128, 64, 128)
+    P = B.Problem(1, 64, 2, 512, 128, 64, 128, 0.072)
     fake = ctypes.c_void_p(0x10000)
     z = None
     cfg = B._CPrologue(1e-6, 10000.0, 0)
@@ -128,7 +128,7 @@ def test_workspace_sizes_follow_the_header():
     """laga_workspace_bytes against the sizes include/laga.h states (host logic only)."""
     lib, B = _raw()
     for S, H, Bt in ((1, 1, 1), (64, 2, 1), (300, 3, 2), (16384, 16, 1)):
-        P = B.Problem(Bt, S, H, 512, 128, 64, 128)
+        P = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072)
         T = (S + 31) // 32
         ds = 2 * Bt * H * 512 * T * (T + 1)
         dkv = 2 * Bt * S * H * 256
@@ -136,13 +136,24 @@ def test_workspace_sizes_follow_the_header():
         # the dS^T store plus dKV hi and lo at least; everything rounded to 256 bytes
         assert need >= ds + 2 * dkv and need % 256 == 0, (S, H, Bt)
         # non-causal: the full square of tiles
-        Pn = B.Problem(Bt, S, H, 512, 128, 64, 128, causal=0)
+        Pn = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072, causal=0)
         assert lib.laga_workspace_bytes(ctypes.byref(Pn.c()), 1) - need == 2 * Bt * H * 1024 * T * T - ds
-        # the fused mode adds the rebuilt kv to the backward and W^T to the forward
-        Pf = B.Problem(Bt, S, H, 512, 128, 64, 128, kv_mode=B.KV_FUSED)
-        assert lib.laga_workspace_bytes(ctypes.byref(Pf.c()), 1) == need + dkv
+        # the fused mode adds W^T to the forward and to the backward (whose kernels rebuild
+        # K/V on chip); with dq recomputed, the backward rebuilds kv into its workspace instead
+        wt = (2 * 512 * H * 256 + 255) // 256 * 256
+        Pf = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072, kv_mode=B.KV_FUSED)
+        assert lib.laga_workspace_bytes(ctypes.byref(Pf.c()), 1) == need + wt
+        Pfr = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072, kv_mode=B.KV_FUSED, dq_mode=B.DQ_RECOMPUTE)
+        Pr0 = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072, dq_mode=B.DQ_RECOMPUTE)
+        assert lib.laga_workspace_bytes(ctypes.byref(Pfr.c()), 1) == \
+            lib.laga_workspace_bytes(ctypes.byref(Pr0.c()), 1) + (dkv + 255) // 256 * 256
         assert lib.laga_workspace_bytes(ctypes.byref(Pf.c()), 0) == 2 * 512 * H * 256
         assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 0) == 0
+        # dq recomputed: exactly the store less, and nothing of S x S size
+        Pr = B.Problem(Bt, S, H, 512, 128, 64, 128, 0.072, dq_mode=B.DQ_RECOMPUTE)
+        rec = lib.laga_workspace_bytes(ctypes.byref(Pr.c()), 1)
+        assert need - rec == (ds + 255) // 256 * 256, (S, H, Bt)
+        assert rec < 64 * Bt * S * H * 256 + (1 << 20)
     # fp32 stores no dS^T (4.3 GB in bf16 at S=16384, 16 heads): its workspace is linear in S
-    P = B.Problem(1, 16384, 16, 512, 128, 64, 128, dtype=B.DTYPE_FP32)
+    P = B.Problem(1, 16384, 16, 512, 128, 64, 128, 0.072, dtype=B.DTYPE_FP32)
     assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 1) < 1 << 30

@@ -4,28 +4,12 @@ import pytest
 
 import laga_inputs as LI
 from oracle import laga as O
-from _util import TOL, dev_inputs, err, f64, problem_for, scaled_err
+from _util import TOL, check_tol, dev_inputs, err, errors, f64, problem_for, scaled_err
 
 pytestmark = pytest.mark.gpu
 
 NAMES = ("dq", "dc_kv", "dk_pe", "dw_kv_b")
 
-
-# dk_pe sums the rope-band gradient of every head; at the first keys it is the small
-# difference of larger per-head terms. A CPU emulation of exactly this path's bf16 rounding
-# points (bf16 K/V, P and dZ as MFMA operands, bf16 out in delta) lands at 1.9-2.2e-2 on it,
-# i.e. the 2e-2 bar is this tensor's bf16 noise floor; it is held to 1.5x that bar.
-DKPE_BF16_TOL = 3e-2
-
-
-def tol_for(name, dtype):
-    return DKPE_BF16_TOL if (name == "dk_pe" and dtype == "bf16") else TOL[dtype]
-
-
-def metric(name):
-    """Token-local tensors are held element-wise to tol * max(1, |ref|); dW, a sum over
-    all tokens, is held to tol * max(1, rms(dW))."""
-    return err if name == "dw_kv_b" else scaled_err
 
 
 def gpu_step(w, d, **kw):
@@ -45,12 +29,11 @@ def check_full(w):
     x = LI.make_inputs(w)
     g, _, _ = gpu_step(w, dev_inputs(w, x))
     ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
-    errs = {k: metric(k)(f64(g[k]), ref[k]) for k in NAMES}
-    rms_errs = {k: err(f64(g[k]), ref[k]) for k in NAMES}
+    errs = {k: errors(k, f64(g[k]), ref[k]) for k in NAMES}
     print(f"{w.name} S={w.seq_len} H={w.n_heads} B={w.batch} causal={w.causal}: " +
-          " ".join(f"{k} {v:.2e} (rms-scaled {rms_errs[k]:.2e})" for k, v in errs.items()))
-    for k, v in errs.items():
-        assert v < tol_for(k, w.dtype), (k, v)
+          " ".join(f"{k} {v[0]:.2e} (rms-scaled {v[1]:.2e})" for k, v in errs.items()))
+    for k in NAMES:
+        check_tol(k, f64(g[k]), ref[k], w.dtype)
 
 
 @pytest.mark.parametrize("S,B,causal", [(256, 1, True), (1, 1, True), (7, 2, True), (100, 1, True),
@@ -61,7 +44,7 @@ def test_tiny_fp32(S, B, causal):
 
 # (288, 3, 1): the large-tile GEMMs with partial tiles (tokens 288 = 256 + 32; dc split
 # over heads; dW over 288 tokens); (264, 2, 2): likewise with batch 2, non-causal.
-@pytest.mark.parametrize("S,H,B,causal", [(2048, 16, 1, True), (1, 1, 1, True), (7, 3, 2, True),
+@pytest.mark.parametrize("S,H,B,causal", [(2048, 16, 1, True), (4096, 16, 1, True), (1, 1, 1, True), (7, 3, 2, True),
                                           (257, 3, 2, True), (300, 2, 1, False), (288, 3, 1, True),
                                           (264, 2, 2, False)])
 def test_v3_bf16(S, H, B, causal):
@@ -88,9 +71,8 @@ def test_s16384_sampled(S):
     tail = w.seq_len - 128
     rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
     for k in ("dq", "dc_kv", "dk_pe"):
-        e = scaled_err(f64(g[k][:, tail:]), rb[k][:, tail:])
-        print(f"S={S} tail rows {k}: {e:.3e}")
-        assert e < tol_for(k, "bf16"), (k, e)
+        e = check_tol(k, f64(g[k][:, tail:]), rb[k][:, tail:], "bf16", f"S={S} tail")
+        print(f"S={S} tail rows {k}: {e[0]:.3e} (rms-scaled {e[1]:.3e})")
     check_invariants(x, g)
 
 
@@ -110,9 +92,8 @@ def test_long_sequence_two_heads():
     tail = S - 96
     rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
     for k in ("dq", "dc_kv", "dk_pe"):
-        e = scaled_err(f64(g[k][:, tail:]), rb[k][:, tail:])
-        print(f"S={S} tail rows {k}: {e:.3e}")
-        assert e < tol_for(k, "bf16"), (k, e)
+        e = check_tol(k, f64(g[k][:, tail:]), rb[k][:, tail:], "bf16", f"S={S} tail")
+        print(f"S={S} tail rows {k}: {e[0]:.3e} (rms-scaled {e[1]:.3e})")
     check_invariants(x, g)
 
 
@@ -205,16 +186,16 @@ def test_rising_scores_exercise_the_online_rescale(dtype):
     x["q"] = LI.round_to(q, dtype)
     g, out, lse = gpu_step(w, dev_inputs(w, x))
     ro, rl = O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **okw(w))
-    errs = {"out": scaled_err(f64(out), ro), "lse": scaled_err(f64(lse), rl)}
+    got = {"out": (f64(out), ro), "lse": (f64(lse), rl)}
     if dtype == "fp32":
         ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
-        errs.update({k: metric(k)(f64(g[k]), ref[k]) for k in NAMES})
+        got.update({k: (f64(g[k]), ref[k]) for k in NAMES})
     print(f"rising scores {dtype}: lse range {rl.min():.1f}..{rl.max():.1f}; " +
-          " ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+          " ".join(f"{k} {errors(k, *v)[0]:.2e}" for k, v in got.items()))
     # the maximum over a row really moves by many rescale thresholds (2^8 in exp2 units)
     assert (rl.max() - rl.min()) / np.log(2.0) > 3 * 8
-    for k, v in errs.items():
-        assert v < tol_for(k, w.dtype), (k, v)
+    for k, v in got.items():
+        check_tol(k, *v, w.dtype)
 
 
 def test_random_shapes():
@@ -242,10 +223,79 @@ def test_s16384_two_heads_against_the_full_oracle():
           "dout": x["dout"][:, :, :2]}
     g2, _, _ = gpu_step(w2, dev_inputs(w2, x2))
     ref = O.attn_bwd(x2["q"], x2["c_kv"], x2["k_pe"], x2["w_kv_b"], x2["dout"], **okw(w2))
-    errs = {"dq": scaled_err(f64(g16["dq"][:, :, :2]), ref["dq"]),
-            "dw_kv_b": err(f64(g16["dw_kv_b"][:, :512]), ref["dw_kv_b"]),
-            "dc_kv": scaled_err(f64(g2["dc_kv"]), ref["dc_kv"]),
-            "dk_pe": scaled_err(f64(g2["dk_pe"]), ref["dk_pe"])}
-    print("S=16384 heads 0-1 vs the full oracle: " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()))
-    for k, v in errs.items():
-        assert v < tol_for(k, "bf16"), (k, v)
+    got = {"dq": (f64(g16["dq"][:, :, :2]), ref["dq"]),
+           "dw_kv_b": (f64(g16["dw_kv_b"][:, :512]), ref["dw_kv_b"]),
+           "dc_kv": (f64(g2["dc_kv"]), ref["dc_kv"]),
+           "dk_pe": (f64(g2["dk_pe"]), ref["dk_pe"])}
+    print("S=16384 heads 0-1 vs the full oracle: " +
+          " ".join(f"{k} {errors(k, *v)[0]:.2e}" for k, v in got.items()))
+    for k, v in got.items():
+        check_tol(k, *v, "bf16")
+
+
+@pytest.mark.parametrize("S,H,B,causal", [(2048, 16, 1, True), (7, 3, 2, True), (300, 2, 1, False),
+                                          (257, 3, 2, True)])
+def test_recompute_mode_against_the_oracle(S, H, B, causal):
+    """dq_mode RECOMPUTE (no S x S buffer): the full oracle comparison, and every gradient
+    but dq bit-identical to the dS^T-store mode (the key-stationary pass is the same
+    arithmetic without the store; dq comes from a pass that recomputes the scores)."""
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    g_store, _, _ = gpu_step(w, d)
+    g, _, _ = gpu_step(w, d, dq_mode=L.DQ_RECOMPUTE)
+    for k in ("dc_kv", "dk_pe", "dw_kv_b"):
+        assert torch.equal(g[k], g_store[k]), k
+    ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+    for k in NAMES:
+        e = check_tol(k, f64(g[k]), ref[k], "bf16", f"recompute S={S}")
+        print(f"recompute S={S} H={H} B={B} causal={causal} {k}: {e[0]:.2e} (rms-scaled {e[1]:.2e})")
+
+
+def test_recompute_mode_s16384():
+    """The benchmark's configuration without the 4.3 GB dS^T store: the workspace is linear
+    in S, dq meets the oracle on sampled rows and the tail, and the other gradients equal
+    the store mode's bit for bit."""
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_train_s16384"]
+    p_store, p_rec = problem_for(w), problem_for(w, dq_mode=L.DQ_RECOMPUTE)
+    ws_store, ws_rec = L.laga_workspace_bytes(p_store, L.OP_BWD), L.laga_workspace_bytes(p_rec, L.OP_BWD)
+    T = (w.seq_len + 31) // 32
+    assert ws_store - ws_rec >= 2 * w.n_heads * 512 * T * (T + 1)
+    assert ws_rec < (1 << 30)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    g_store, _, _ = gpu_step(w, d)
+    g, _, _ = gpu_step(w, d, dq_mode=L.DQ_RECOMPUTE)
+    for k in ("dc_kv", "dk_pe", "dw_kv_b"):
+        assert torch.equal(g[k], g_store[k]), k
+    S = w.seq_len
+    rows = [0, 1, 100, 5000, S - 1]
+    r = O.attn_fwd_rows(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], rows, dout=x["dout"],
+                        n_heads=16, d_nope=128, d_v=128, scale=w.scale)
+    check_tol("dq", f64(g["dq"][:, rows]), r["dq"], "bf16", "recompute sampled rows")
+    tail = S - 128
+    rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
+    check_tol("dq", f64(g["dq"][:, tail:]), rb["dq"][:, tail:], "bf16", "recompute tail")
+    # both dq passes compute the same sums in different fp32 orders
+    diff = (g["dq"].float() - g_store["dq"].float()).abs().max().item()
+    print(f"recompute vs store dq max |diff| {diff:.3e}")
+    assert diff < 2e-2
+
+
+def test_s16384_sixteen_heads_against_the_full_oracle():
+    """The benchmark's configuration (S=16384, 16 heads, as bench.py launches it) against the
+    full oracle on every element of every gradient: dq, dW and the head sums dc_kv and dk_pe
+    (whose first keys, seen by every query of every head, carry the largest error)."""
+    w = LI.WORKLOADS["v3_train_s16384"]
+    x = LI.make_inputs(w)
+    g, _, _ = gpu_step(w, dev_inputs(w, x))
+    ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], chunk=1024, **okw(w))
+    errs = {k: errors(k, f64(g[k]), ref[k]) for k in NAMES}
+    print("S=16384 H=16 vs the full oracle: " +
+          " ".join(f"{k} {v[0]:.2e} (rms-scaled {v[1]:.2e})" for k, v in errs.items()))
+    for k in NAMES:
+        check_tol(k, f64(g[k]), ref[k], "bf16")
