@@ -85,7 +85,8 @@ typedef enum {
   LAGA_ERR_UNSUPPORTED = 3, /* dims/dtype/mode/size the library has no kernel for */
   LAGA_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
   LAGA_ERR_WORKSPACE = 5,   /* workspace smaller than laga_workspace_bytes() */
-  LAGA_ERR_DEVICE = 6       /* the HIP runtime reported an error at launch */
+  LAGA_ERR_DEVICE = 6,      /* the HIP runtime reported an error at launch */
+  LAGA_ERR_SCRATCH = 7      /* laga_attn_bwd_noalloc: workspace need above its fixed array */
 } laga_status_t;
 
 typedef enum { LAGA_DTYPE_BF16 = 0, LAGA_DTYPE_FP32 = 1 } laga_dtype_t;
@@ -186,6 +187,28 @@ LAGA_API laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p,
                                            void* dq, float* dc_kv, float* dk_pe,
                                            float* dw_kv_b, void* workspace,
                                            size_t workspace_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): laga_attn_bwd without a workspace
+ * argument. Same arguments, results and stream semantics as laga_attn_bwd; its
+ * workspace is a static device array of LAGA_NOALLOC_SCRATCH_BYTES that the library
+ * holds on each GPU it runs on until the process ends (the entry point itself calls no
+ * allocator). Limits and behaviour:
+ *   - a problem whose laga_workspace_bytes(p, LAGA_OP_BWD) exceeds the array returns
+ *     LAGA_ERR_SCRATCH before any launch (e.g. bf16 V3 heads, H = 16: S up to 2048
+ *     with dq_mode RECOMPUTE, up to 1024 with FROM_STORE);
+ *   - the array belongs to the current device; `stream` (NULL: the default stream) must
+ *     be a stream of that device, else LAGA_ERR_DEVICE;
+ *   - every call on one GPU uses the same array, and a call leaves its contents behind:
+ *     calls that can overlap on one GPU (on different streams, or from different host
+ *     threads without ordering) race and must not be issued. */
+#define LAGA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+LAGA_API laga_status_t laga_attn_bwd_noalloc(const laga_problem_t* p, const void* q,
+                                             const void* c_kv, const void* k_pe,
+                                             const void* w_kv_b, const void* kv, const void* out,
+                                             const float* lse, const void* dout, void* dq,
+                                             float* dc_kv, float* dk_pe, float* dw_kv_b,
+                                             void* stream);
 
 /* ---- Producers around the latent all-gather ---------------------------------
  * The per-token steps that make this block's inputs and consume its gradients

@@ -7,12 +7,12 @@ library is missing, importing the binding raises.
 """
 from .binding import (LagaError, Problem, DTYPE_BF16, DTYPE_FP32, DQ_FROM_STORE, DQ_RECOMPUTE, KV_MATERIALIZED,
                       KV_FUSED, OP_FWD, OP_BWD, OP_PROLOGUE_BWD, BWD_PREPARE, BWD_DKDV, BWD_DQ,
-                      BWD_FINISH, laga_abi_version, laga_attn_bwd, laga_attn_bwd_stage,
+                      BWD_FINISH, laga_abi_version, laga_attn_bwd, laga_attn_bwd_noalloc, laga_attn_bwd_stage,
                       laga_attn_fwd, laga_prologue_bwd, laga_prologue_fwd, laga_reconstruct_kv,
-                      laga_status_string, laga_workspace_bytes, lib_path)
+                      laga_status_string, laga_workspace_bytes, lib_path, NOALLOC_SCRATCH_BYTES)
 
 __all__ = ["LagaError", "Problem", "DTYPE_BF16", "DTYPE_FP32", "DQ_FROM_STORE", "DQ_RECOMPUTE", "KV_MATERIALIZED",
            "KV_FUSED", "OP_FWD", "OP_BWD", "OP_PROLOGUE_BWD", "BWD_PREPARE", "BWD_DKDV", "BWD_DQ",
-           "BWD_FINISH", "laga_abi_version", "laga_attn_bwd", "laga_attn_bwd_stage",
+           "BWD_FINISH", "laga_abi_version", "laga_attn_bwd", "laga_attn_bwd_noalloc", "laga_attn_bwd_stage",
            "laga_attn_fwd", "laga_prologue_bwd", "laga_prologue_fwd", "laga_reconstruct_kv",
-           "laga_status_string", "laga_workspace_bytes", "lib_path"]
+           "laga_status_string", "laga_workspace_bytes", "lib_path", "NOALLOC_SCRATCH_BYTES"]

@@ -23,7 +23,8 @@ OP_FWD, OP_BWD, OP_PROLOGUE_BWD = 0, 1, 2
 BWD_PREPARE, BWD_DKDV, BWD_DQ, BWD_FINISH = 0, 1, 2, 3
 
 _STATUS = {0: "LAGA_OK", 1: "LAGA_ERR_NULL", 2: "LAGA_ERR_SHAPE", 3: "LAGA_ERR_UNSUPPORTED",
-           4: "LAGA_ERR_ALIGN", 5: "LAGA_ERR_WORKSPACE", 6: "LAGA_ERR_DEVICE"}
+           4: "LAGA_ERR_ALIGN", 5: "LAGA_ERR_WORKSPACE", 6: "LAGA_ERR_DEVICE", 7: "LAGA_ERR_SCRATCH"}
+NOALLOC_SCRATCH_BYTES = 128 << 20  # LAGA_NOALLOC_SCRATCH_BYTES
 
 
 class LagaError(RuntimeError):
@@ -95,6 +96,8 @@ def _load():
     L.laga_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.laga_attn_bwd.restype = ctypes.c_int
     L.laga_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.laga_attn_bwd_noalloc.restype = ctypes.c_int
+    L.laga_attn_bwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.laga_attn_bwd_stage.restype = ctypes.c_int
     L.laga_attn_bwd_stage.argtypes = [ctypes.c_int, P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       ctypes.c_size_t, vp]
@@ -200,7 +203,8 @@ def _bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe, dw
             _ptr(dq, "dq", sh["dq"], dt), _ptr(dc_kv, "dc_kv", sh["dc_kv"], torch.float32),
             _ptr(dk_pe, "dk_pe", sh["dk_pe"], torch.float32),
             _ptr(dw_kv_b, "dw_kv_b", sh["dw_kv_b"], torch.float32),
-            _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size())
+            _ptr(workspace, "workspace", required=False),
+            0 if workspace is None else workspace.numel() * workspace.element_size())
 
 
 def _bwd_outputs(p, dev, dq, dc_kv, dk_pe, dw_kv_b, workspace):
@@ -223,6 +227,20 @@ def laga_attn_bwd(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None
     dq, dc_kv, dk_pe, dw_kv_b, workspace = _bwd_outputs(p, q.device, dq, dc_kv, dk_pe, dw_kv_b, workspace)
     _check(_lib.laga_attn_bwd(*_bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe,
                                          dw_kv_b, workspace), _stream(stream)), "laga_attn_bwd")
+    return dq, dc_kv, dk_pe, dw_kv_b
+
+
+def laga_attn_bwd_noalloc(p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq=None, dc_kv=None,
+                          dk_pe=None, dw_kv_b=None, stream=None):
+    """laga_attn_bwd with the library's fixed device scratch array as its workspace (for
+    callers that cannot allocate; LagaError LAGA_ERR_SCRATCH above its size). Outputs not
+    supplied are allocated here, as for laga_attn_bwd."""
+    dev = q.device
+    dq, dc_kv, dk_pe, dw_kv_b = [t if t is not None else _new(p, n, dt, dev) for t, n, dt in (
+        (dq, "dq", p.torch_dtype), (dc_kv, "dc_kv", torch.float32), (dk_pe, "dk_pe", torch.float32),
+        (dw_kv_b, "dw_kv_b", torch.float32))]
+    args = _bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe, dw_kv_b, None)
+    _check(_lib.laga_attn_bwd_noalloc(*args[:-2], _stream(stream)), "laga_attn_bwd_noalloc")
     return dq, dc_kv, dk_pe, dw_kv_b
 
 

@@ -3,6 +3,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "laga.h"
 #include "kernels.hpp"
 #include "bwd_common.hpp"
@@ -130,6 +132,39 @@ laga_status_t reconstruct_t(const Dims& d, const void* c, const void* w, void* k
 
 }  // namespace
 
+// Device memory of laga_attn_bwd_noalloc: the backward's workspace for callers that
+// cannot allocate. Each GPU the library runs on holds its own copy until the process
+// ends. Host code never uses this name as an address (on the host it is only a handle
+// for hipGetSymbolAddress); kernels get the per-device address found below.
+static __device__ __align__(256) unsigned char scratch[LAGA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];  // device address of `scratch` on each device, once known
+
+// Address of `scratch` on the current device (looked up once per device, with that device
+// current). The stream must belong to the current device.
+laga_status_t scratch_address(hipStream_t st, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LAGA_ERR_DEVICE;
+  if (st) {
+    hipDevice_t sd = -1;
+    if (hipStreamGetDevice(st, &sd) != hipSuccess || sd != dev) return LAGA_ERR_DEVICE;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return LAGA_ERR_DEVICE;
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return LAGA_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int laga_abi_version(void) { return LAGA_ABI_VERSION; }
@@ -143,6 +178,9 @@ const char* laga_status_string(laga_status_t s) {
     case LAGA_ERR_ALIGN: return "LAGA_ERR_ALIGN: a pointer is not 16-byte aligned";
     case LAGA_ERR_WORKSPACE: return "LAGA_ERR_WORKSPACE: workspace smaller than laga_workspace_bytes()";
     case LAGA_ERR_DEVICE: return "LAGA_ERR_DEVICE: the HIP runtime reported a launch error";
+    case LAGA_ERR_SCRATCH:
+      return "LAGA_ERR_SCRATCH: the problem needs more workspace than the no-alloc entry point's fixed "
+             "device array holds (LAGA_NOALLOC_SCRATCH_BYTES)";
   }
   return "unknown laga_status_t";
 }
@@ -323,6 +361,22 @@ laga_status_t laga_attn_bwd(const laga_problem_t* p, const void* q, const void* 
     if (s != LAGA_OK) return s;
   }
   return LAGA_OK;
+}
+
+laga_status_t laga_attn_bwd_noalloc(const laga_problem_t* p, const void* q, const void* c_kv, const void* k_pe,
+                                    const void* w_kv_b, const void* kv, const void* out, const float* lse,
+                                    const void* dout, void* dq, float* dc_kv, float* dk_pe, float* dw_kv_b,
+                                    void* stream) {
+  Dims d;
+  laga_status_t s = validate(p, &d);
+  if (s != LAGA_OK) return s;
+  if (bwd_layout(p, d).total > (size_t)LAGA_NOALLOC_SCRATCH_BYTES) return LAGA_ERR_SCRATCH;
+  void* ws = nullptr;
+  s = scratch_address((hipStream_t)stream, &ws);
+  if (s != LAGA_OK) return s;
+  // nothing in the workspace needs to start at zero: every stage writes what a later one reads
+  return laga_attn_bwd(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq, dc_kv, dk_pe, dw_kv_b, ws,
+                       (size_t)LAGA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"
