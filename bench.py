@@ -14,7 +14,9 @@ Beside the headline step (dq from the stored dS^T), the same line reports the st
 dq recomputed (no S x S buffer), the step with K/V rebuilt on chip from the latent
 (kv_mode FUSED; the forward's executed and algorithmic TFLOP/s), the step at
 S = 2048, 4096 and 8192, the producers around the all-gather, the clock under load and
-the CPU oracle (fp32 timed, fp64 beside it) on a bounded sample of the workload.
+the output projection W_o after the out all-to-all (Alg. 1 step 7) on one rank's
+share, and the CPU oracle (fp32 timed, fp64 beside it) on a bounded sample of the
+workload.
 """
 from __future__ import annotations
 
@@ -43,7 +45,7 @@ def parse():
     ap.add_argument("--heads", type=int, default=None,
                     help="override the shard's head count (sweep over SP degrees); default 16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=4,
+    ap.add_argument("--cpu-heads", type=int, default=8,
                     help="heads of the workload the CPU oracle runs as its bounded sample")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip timing the step as one captured HIP graph")
@@ -300,6 +302,43 @@ def gpu_bench(w, steps, warmup, clock_probe_s=0.0, graph=False, extras=True):
                         torch.equal(a, b) for a, b in zip((fu.dc, fu.dkpe, fu.dw), grads_m)))}
     del fu
     torch.cuda.empty_cache()
+    return res
+
+
+def out_proj_bench(w, steps, warmup, sp=8, d_model=7168):
+    """The block's consumer, W_o of Alg. 1 step 7 (forward and backward), on one rank's share
+    after the out all-to-all: S/sp tokens with every head of the layer (n_h = sp x the
+    shard's heads), timed apart from the step. MFMA-bound: reported against the bf16 peak."""
+    import torch
+    import laga_inputs as LI
+    import paper_2607_17644_amd as L
+    T, nh = w.seq_len // sp, w.n_heads * sp
+    x = LI.make_out_proj_inputs(T, nh, w.d_v, d_model)
+    dev = torch.device("cuda:0")
+    d = {k: torch.from_numpy(v).to(torch.bfloat16).to(dev) for k, v in x.items()}
+    p = L.OutProj(T, nh, w.d_v, d_model)
+    sh = p.shapes()
+    y = torch.empty(sh["y"], dtype=torch.bfloat16, device=dev)
+    d_out = torch.empty(sh["d_out"], dtype=torch.bfloat16, device=dev)
+    dw = torch.empty(sh["dw_o"], dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, L.laga_out_proj_workspace_bytes(p)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    res = {"tokens": T, "n_heads": nh, "d_v": w.d_v, "d_model": d_model}
+    fl = 2.0 * T * nh * w.d_v * d_model
+    for name, fn, f in (("fwd", lambda: L.laga_out_proj_fwd(p, d["out"], d["w_o"], y=y, stream=stream), fl),
+                        ("bwd", lambda: L.laga_out_proj_bwd(p, d["out"], d["w_o"], d["dy"], d_out=d_out, dw_o=dw,
+                                                            workspace=ws, stream=stream), 2 * fl)):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        tf = f / (ms * 1e-3) / 1e12
+        res[name] = {"ms": round(ms, 4), "tflops": round(tf, 1), "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)}
     return res
 
 
@@ -574,6 +613,8 @@ def main():
     if not a.no_extras and a.seq_len is None:
         line["sweep"] = sweep_bench(w, (2048, 4096, 8192), a.steps, a.warmup)
     line["prologue_outside_step"] = g.get("prologue")
+    if not a.no_extras and a.seq_len is None and a.heads is None:
+        line["out_proj_outside_step"] = out_proj_bench(w, a.steps, a.warmup)
     line["clock_under_load"] = g.get("clock")
     line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)

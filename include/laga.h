@@ -15,6 +15,8 @@
  *   laga_attn_bwd       : the per-rank backward (Section 5.2 covers the
  *                         collectives around it): dq, the head-shard partials
  *                         dc_kv and dk_pe, and the W_kv_b shard gradient dW
+ *   laga_out_proj_fwd/_bwd : Alg. 1 step 7, the output projection W_o after the
+ *                         out all-to-all, and its backward
  *
  * Layouts (all row-major, contiguous, device memory, 16-byte aligned):
  *   c_kv   [B, S, d_c]                     element dtype
@@ -259,6 +261,40 @@ LAGA_API laga_status_t laga_prologue_bwd(const laga_problem_t* p, const laga_pro
                                          const float* dk_pe, void* dq, float* d_latent_raw,
                                          float* d_kpe_raw, float* d_gamma, void* workspace,
                                          size_t workspace_bytes, void* stream);
+
+/* ---- Consumer of the block: the output projection (Alg. 1 step 7) -------------
+ * After the out all-to-all (Alg. 1 step 6) a rank holds the attention output of every
+ * head for its tokens; step 7 returns W_o(reshape(out)):
+ *   out  [T, n_heads, d_v]    element dtype (head-major: feature f = h * d_v + e)
+ *   w_o  [F, d_model]         element dtype, F = n_heads * d_v (in x out)
+ *   y    [T, d_model]         element dtype:  y = reshape(out) @ w_o
+ * and its backward given dy [T, d_model] (element dtype):
+ *   d_out [T, n_heads, d_v]   element dtype:  d_out = dy @ w_o^T
+ *   dw_o  [F, d_model]        fp32:           dw_o = reshape(out)^T @ dy (over all T tokens,
+ *                             in a fixed order: bitwise repeatable)
+ * fp32 accumulation throughout. T is whatever rows the caller has: a rank's S/P tokens
+ * after the all-to-all, or B*S on one rank. Validation as for the attention calls: NULL
+ * problem or pointer -> LAGA_ERR_NULL; a non-positive size -> LAGA_ERR_SHAPE; F or d_model
+ * not a multiple of 16, an unknown dtype, reserved != 0, or T*F, T*d_model or F*d_model
+ * not below 2^31 -> LAGA_ERR_UNSUPPORTED; misaligned -> LAGA_ERR_ALIGN; workspace smaller
+ * than laga_out_proj_workspace_bytes() -> LAGA_ERR_WORKSPACE. */
+typedef struct {
+  int64_t tokens;  /* T */
+  int64_t n_heads; /* every head of the layer */
+  int64_t d_v;
+  int64_t d_model; /* D */
+  int32_t dtype;   /* laga_dtype_t */
+  int32_t reserved; /* must be 0 */
+} laga_out_proj_t;
+
+LAGA_API laga_status_t laga_out_proj_fwd(const laga_out_proj_t* p, const void* out, const void* w_o,
+                                         void* y, void* stream);
+LAGA_API laga_status_t laga_out_proj_bwd(const laga_out_proj_t* p, const void* out, const void* w_o,
+                                         const void* dy, void* d_out, float* dw_o, void* workspace,
+                                         size_t workspace_bytes, void* stream);
+/* Workspace of laga_out_proj_bwd (partial sums of dw_o over token ranges); 0 if none is
+ * needed or p is invalid. */
+LAGA_API size_t laga_out_proj_workspace_bytes(const laga_out_proj_t* p);
 
 /* Workspace bytes that op (laga_op_t) needs for problem p; 0 if none or if p
  * is invalid (check with the entry point itself for the error code). For the

@@ -201,3 +201,18 @@ def make_prologue_inputs(w: Workload, seed_offset: int = 1) -> dict:
         "dk_pe": dk.astype(np.float32),
         "dq": round_to(dq, w.dtype),
     }
+
+
+def make_out_proj_inputs(tokens: int, n_heads: int, d_v: int, d_model: int, dtype: str = "bf16",
+                         seed: int = 0) -> dict:
+    """Inputs of the output projection (Alg. 1 step 7) and its backward: the gathered
+    attention output out [T, n_heads, d_v] (attention outputs are convex combinations of
+    value rows, so below unit scale: N(0, 0.25^2)), the weight w_o [n_heads * d_v, d_model]
+    ~ N(0, 1 / (n_heads * d_v)) and the upstream gradient dy [T, d_model] ~ N(0, 1), each
+    rounded to ``dtype``. Drawn from its own stream (seed + 2), in that order."""
+    rng = np.random.Generator(np.random.PCG64(seed + 2))
+    F = n_heads * d_v
+    out = 0.25 * rng.standard_normal((tokens, n_heads, d_v))
+    w = rng.standard_normal((F, d_model)) / np.sqrt(F)
+    dy = rng.standard_normal((tokens, d_model))
+    return {"out": round_to(out, dtype), "w_o": round_to(w, dtype), "dy": round_to(dy, dtype)}

@@ -41,6 +41,34 @@ class _CProblem(ctypes.Structure):
                 ("dq_mode", ctypes.c_int32)]
 
 
+class _COutProj(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_int64), ("n_heads", ctypes.c_int64), ("d_v", ctypes.c_int64),
+                ("d_model", ctypes.c_int64), ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+@dataclasses.dataclass
+class OutProj:
+    """Mirror of laga_out_proj_t (Alg. 1 step 7: y = reshape(out) @ w_o)."""
+    tokens: int
+    n_heads: int
+    d_v: int
+    d_model: int
+    dtype: int = DTYPE_BF16
+    reserved: int = 0
+
+    def c(self) -> _COutProj:
+        return _COutProj(self.tokens, self.n_heads, self.d_v, self.d_model, self.dtype, self.reserved)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == DTYPE_BF16 else torch.float32
+
+    def shapes(self) -> dict:
+        T, F = self.tokens, self.n_heads * self.d_v
+        return {"out": (T, self.n_heads, self.d_v), "w_o": (F, self.d_model), "y": (T, self.d_model),
+                "dy": (T, self.d_model), "d_out": (T, self.n_heads, self.d_v), "dw_o": (F, self.d_model)}
+
+
 class _CPrologue(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_float), ("rope_base", ctypes.c_float), ("position_offset", ctypes.c_int64)]
 
@@ -101,6 +129,13 @@ def _load():
     L.laga_attn_bwd_stage.restype = ctypes.c_int
     L.laga_attn_bwd_stage.argtypes = [ctypes.c_int, P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       ctypes.c_size_t, vp]
+    O = ctypes.POINTER(_COutProj)
+    L.laga_out_proj_fwd.restype = ctypes.c_int
+    L.laga_out_proj_fwd.argtypes = [O, vp, vp, vp, vp]
+    L.laga_out_proj_bwd.restype = ctypes.c_int
+    L.laga_out_proj_bwd.argtypes = [O, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.laga_out_proj_workspace_bytes.restype = ctypes.c_size_t
+    L.laga_out_proj_workspace_bytes.argtypes = [O]
     Q = ctypes.POINTER(_CPrologue)
     L.laga_prologue_fwd.restype = ctypes.c_int
     L.laga_prologue_fwd.argtypes = [P, Q, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -251,6 +286,40 @@ def laga_attn_bwd_stage(stage: int, p: Problem, q, c_kv, k_pe, w_kv_b, kv, out, 
     _check(_lib.laga_attn_bwd_stage(stage, *_bwd_args(p, q, c_kv, k_pe, w_kv_b, kv, out, lse, dout, dq,
                                                        dc_kv, dk_pe, dw_kv_b, workspace), _stream(stream)),
            "laga_attn_bwd_stage")
+
+
+def laga_out_proj_workspace_bytes(p: OutProj) -> int:
+    return int(_lib.laga_out_proj_workspace_bytes(ctypes.byref(p.c())))
+
+
+def laga_out_proj_fwd(p: OutProj, out, w_o, y=None, stream=None):
+    """Alg. 1 step 7: y = reshape(out) @ w_o; out [T, n_heads, d_v], w_o [F, d_model]."""
+    sh, dt = p.shapes(), p.torch_dtype
+    if y is None:
+        y = torch.empty(sh["y"], dtype=dt, device=out.device)
+    _check(_lib.laga_out_proj_fwd(ctypes.byref(p.c()), _ptr(out, "out", sh["out"], dt),
+                                  _ptr(w_o, "w_o", sh["w_o"], dt), _ptr(y, "y", sh["y"], dt), _stream(stream)),
+           "laga_out_proj_fwd")
+    return y
+
+
+def laga_out_proj_bwd(p: OutProj, out, w_o, dy, d_out=None, dw_o=None, workspace=None, stream=None):
+    """Backward of laga_out_proj_fwd: (d_out in the element dtype, dw_o in fp32)."""
+    sh, dt = p.shapes(), p.torch_dtype
+    dev = out.device
+    if d_out is None:
+        d_out = torch.empty(sh["d_out"], dtype=dt, device=dev)
+    if dw_o is None:
+        dw_o = torch.empty(sh["dw_o"], dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(1, laga_out_proj_workspace_bytes(p)), dtype=torch.uint8, device=dev)
+    _check(_lib.laga_out_proj_bwd(ctypes.byref(p.c()), _ptr(out, "out", sh["out"], dt),
+                                  _ptr(w_o, "w_o", sh["w_o"], dt), _ptr(dy, "dy", sh["dy"], dt),
+                                  _ptr(d_out, "d_out", sh["d_out"], dt),
+                                  _ptr(dw_o, "dw_o", sh["dw_o"], torch.float32), _ptr(workspace, "workspace"),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "laga_out_proj_bwd")
+    return d_out, dw_o
 
 
 def laga_prologue_fwd(p: Problem, latent_raw, kpe_raw, q=None, gamma=None, eps=1e-6, rope_base=10000.0,

@@ -63,10 +63,11 @@ bool stores_ds(const laga_problem_t* p) {
   return p->dtype == LAGA_DTYPE_BF16 && is_v3(p) && p->dq_mode == LAGA_DQ_FROM_STORE;
 }
 // Fused mode without kv: the key-stationary and dQ kernels rebuild K/V tiles on chip from
-// c_kv and W_kv_b^T (bf16 with 192/128-wide heads, dq from the store); other problems
-// rebuild kv once into the workspace and run the materialised kernels.
+// c_kv and W_kv_b^T (bf16 with 192/128-wide heads, dq from the store, d_c a multiple of
+// 128 up to kFusedMaxDc); other problems rebuild kv once into the workspace and run the
+// materialised kernels.
 bool kv_on_chip(const laga_problem_t* p) {
-  return p->kv_mode == LAGA_KV_FUSED && stores_ds(p) && p->d_c <= kFusedMaxDc;
+  return p->kv_mode == LAGA_KV_FUSED && stores_ds(p) && p->d_c <= kFusedMaxDc && p->d_c % 128 == 0;
 }
 int s_pad(int S) { return (S + kRowPad - 1) / kRowPad * kRowPad; }
 BwdWs bwd_layout(const laga_problem_t* p, const Dims& d) {
@@ -123,6 +124,30 @@ PrologueArgs prologue_args(const laga_problem_t* p, const laga_prologue_t* cfg, 
   a.log2_base = log2((double)cfg->rope_base);
   (void)p;
   return a;
+}
+
+// Output projection (Alg. 1 step 7): sizes, validation, workspace.
+struct OutDims {
+  int T, F, D;
+};
+laga_status_t validate_out_proj(const laga_out_proj_t* p, OutDims* d) {
+  if (!p) return LAGA_ERR_NULL;
+  if (p->tokens <= 0 || p->n_heads <= 0 || p->d_v <= 0 || p->d_model <= 0) return LAGA_ERR_SHAPE;
+  if (p->reserved != 0 || (p->dtype != LAGA_DTYPE_BF16 && p->dtype != LAGA_DTYPE_FP32)) return LAGA_ERR_UNSUPPORTED;
+  const int64_t F = p->n_heads * p->d_v;
+  if (F % 16 != 0 || p->d_model % 16 != 0) return LAGA_ERR_UNSUPPORTED;
+  if (F >= kMaxElems || p->tokens * F >= kMaxElems || p->tokens * p->d_model >= kMaxElems ||
+      F * p->d_model >= kMaxElems)
+    return LAGA_ERR_UNSUPPORTED;
+  d->T = (int)p->tokens; d->F = (int)F; d->D = (int)p->d_model;
+  return LAGA_OK;
+}
+int out_proj_splits(const laga_out_proj_t* p, const OutDims& d) {
+  return gemm_tn_splits(d.F, d.D, d.T, p->dtype == LAGA_DTYPE_BF16 ? 2 : 4);
+}
+size_t out_proj_ws_bytes(const laga_out_proj_t* p, const OutDims& d) {
+  const int n = out_proj_splits(p, d);
+  return n > 1 ? round_up(sizeof(float) * (size_t)n * d.F * d.D) : 0;
 }
 
 template <typename T>
@@ -235,6 +260,52 @@ laga_status_t laga_prologue_bwd(const laga_problem_t* p, const laga_prologue_t* 
   a.partial = gamma ? (float*)workspace : nullptr;
   hipStream_t st = (hipStream_t)stream;
   return from_hip(p->dtype == LAGA_DTYPE_BF16 ? launch_prologue_bwd<bf16>(a, st) : launch_prologue_bwd<float>(a, st));
+}
+
+size_t laga_out_proj_workspace_bytes(const laga_out_proj_t* p) {
+  OutDims d;
+  if (validate_out_proj(p, &d) != LAGA_OK) return 0;
+  return out_proj_ws_bytes(p, d);
+}
+
+laga_status_t laga_out_proj_fwd(const laga_out_proj_t* p, const void* out, const void* w_o, void* y, void* stream) {
+  OutDims d;
+  laga_status_t s = validate_out_proj(p, &d);
+  if (s != LAGA_OK) return s;
+  if (!out || !w_o || !y) return LAGA_ERR_NULL;
+  if (misaligned(out) || misaligned(w_o) || misaligned(y)) return LAGA_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  // y[T][D] = out[T][F] @ w_o[F][D]: the up-projection's GEMM (w_o k-strided)
+  return from_hip(p->dtype == LAGA_DTYPE_BF16
+                      ? launch_reconstruct<bf16>((const bf16*)out, (const bf16*)w_o, (bf16*)y, d.T, d.D, d.F, st)
+                      : launch_reconstruct<float>((const float*)out, (const float*)w_o, (float*)y, d.T, d.D, d.F, st));
+}
+
+laga_status_t laga_out_proj_bwd(const laga_out_proj_t* p, const void* out, const void* w_o, const void* dy,
+                                void* d_out, float* dw_o, void* workspace, size_t workspace_bytes, void* stream) {
+  OutDims d;
+  laga_status_t s = validate_out_proj(p, &d);
+  if (s != LAGA_OK) return s;
+  if (!out || !w_o || !dy || !d_out || !dw_o) return LAGA_ERR_NULL;
+  if (misaligned(out) || misaligned(w_o) || misaligned(dy) || misaligned(d_out) || misaligned(dw_o))
+    return LAGA_ERR_ALIGN;
+  const size_t need = out_proj_ws_bytes(p, d);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return LAGA_ERR_WORKSPACE;
+  if (need > 0 && misaligned(workspace)) return LAGA_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  const int ns = out_proj_splits(p, d);
+  hipError_t e;
+  if (p->dtype == LAGA_DTYPE_BF16) {
+    // d_out[T][F] = dy[T][D] @ w_o^T (w_o stored [F][D]: k-contiguous); dw_o[F][D] = out^T @ dy
+    e = launch_gemm_nt<bf16>((const bf16*)dy, (const bf16*)w_o, (bf16*)d_out, d.T, d.F, d.D, st);
+    if (e == hipSuccess)
+      e = launch_gemm_tn<bf16>((const bf16*)out, (const bf16*)dy, dw_o, (float*)workspace, d.F, d.D, d.T, ns, st);
+  } else {
+    e = launch_gemm_nt<float>((const float*)dy, (const float*)w_o, (float*)d_out, d.T, d.F, d.D, st);
+    if (e == hipSuccess)
+      e = launch_gemm_tn<float>((const float*)out, (const float*)dy, dw_o, (float*)workspace, d.F, d.D, d.T, ns, st);
+  }
+  return from_hip(e);
 }
 
 laga_status_t laga_reconstruct_kv(const laga_problem_t* p, const void* c_kv, const void* w_kv_b, void* kv,

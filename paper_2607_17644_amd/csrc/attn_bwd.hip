@@ -418,11 +418,20 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     f32x16 acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[b] = f32x16{};
-    for (int ks = 0; ks < dc / 16; ++ks) {
-      const frag_t<T> cf = *reinterpret_cast<const frag_t<T>*>(cr + ks * 16);
+    // groups of four 16-wide steps (d_c % 128 == 0): 36 loads in flight, then 32 MFMAs
+    for (int k0 = 0; k0 < dc / 16; k0 += 4) {
+      frag_t<T> cf[4], wf[4][NB];
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        mma(acc[b], *reinterpret_cast<const frag_t<T>*>(wt + (size_t)b * 32 * dc + ks * 16), cf);
+      for (int j = 0; j < 4; ++j) {
+        cf[j] = *reinterpret_cast<const frag_t<T>*>(cr + (k0 + j) * 16);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          wf[j][b] = *reinterpret_cast<const frag_t<T>*>(wt + (size_t)b * 32 * dc + (k0 + j) * 16);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) mma(acc[b], wf[j][b], cf[j]);
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b)

@@ -346,8 +346,16 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
       const int key = min(kt + 32 * rk + n, S - 1);
       const T* cr = cg + (size_t)key * dc;
       f32x16 acc = f32x16{};
-      for (int ks = 0; ks < dc / 16; ++ks)
-        mma(acc, *reinterpret_cast<const frag_t<T>*>(wt + ks * 16), *reinterpret_cast<const frag_t<T>*>(cr + ks * 16));
+      for (int k0 = 0; k0 < dc / 16; k0 += 8) {  // d_c % 128 == 0: 16 loads in flight, then 8 MFMAs
+        frag_t<T> wa[8], cb[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          wa[j] = *reinterpret_cast<const frag_t<T>*>(wt + (k0 + j) * 16);
+          cb[j] = *reinterpret_cast<const frag_t<T>*>(cr + (k0 + j) * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) mma(acc, wa[j], cb[j]);
+      }
       T* dst = sK + (32 * rk + n) * KP * 8 + rb * 32 + 8 * g;
       *reinterpret_cast<bf16x8*>(dst) = acc_to_frag<T>(acc, 0);
       *reinterpret_cast<bf16x8*>(dst + 16) = acc_to_frag<T>(acc, 1);

@@ -571,6 +571,64 @@ hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float
   return hipGetLastError();
 }
 
+template <typename T>
+hipError_t launch_gemm_nt(const T* a, const T* w, T* c, int M, int N, int K, hipStream_t st) {
+  // c[M][N] = a[M][K] @ w^T, w stored [N][K] (both k-contiguous); element-dtype output
+  using G = GemmCfg<T>;
+  if constexpr (sizeof(T) == 2) {
+    if (gemm_big_ok(M, N, K, K, (size_t)M * K, (size_t)N * K)) {
+      gemm_big_kernel<256, 256, false, false, 0, bf16><<<grid_tiles(M, N, 256, 256), 256, 0, st>>>(
+          a, w, nullptr, c, M, N, K, K, K, N, K, 0);
+      return hipGetLastError();
+    }
+  }
+  gemm_kernel<T, T, false, false, G::BM, G::BN, G::BK, 0><<<dim3(grid_tiles(M, N, G::BM, G::BN), 1, 1), kThreads,
+                                                              0, st>>>(a, w, nullptr, c, M, N, K, K, K, N, K, 0);
+  return hipGetLastError();
+}
+
+int gemm_tn_splits(int M, int N, int K, int esize) {
+  const bool big = esize == 2 && gemm_big_ok(M, N, K, kGK, (size_t)K * M, (size_t)K * N);
+  const int tiles = big ? grid_tiles(M, N, 256, 256) : grid_tiles(M, N, GemmCfg<bf16>::BM, GemmCfg<bf16>::BN);
+  const int want = big ? 256 : kMinGemmBlocks;
+  int n = (want + tiles - 1) / tiles;
+  const int max_split = (K + 511) / 512;
+  return n < 1 ? 1 : (n > max_split ? max_split : n);
+}
+
+template <typename T>
+hipError_t launch_gemm_tn(const T* a, const T* b, float* c, float* partial, int M, int N, int K, int nsplit,
+                          hipStream_t st) {
+  // c[M][N] = a^T @ b with a stored [K][M] and b [K][N] (both k-strided), fp32 output; the
+  // contraction split into nsplit ranges of whole 32-index stages, summed in ascending order
+  using G = GemmCfg<T>;
+  const int split = ((K + nsplit - 1) / nsplit + 31) / 32 * 32;
+  const int nz = (K + split - 1) / split;
+  float* target = nz == 1 ? c : partial;
+  bool done = false;
+  if constexpr (sizeof(T) == 2) {
+    if (gemm_big_ok(M, N, K, split, (size_t)K * M, (size_t)K * N)) {
+      gemm_big_kernel<256, 256, true, true, 0, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 256, 0, st>>>(
+          a, b, nullptr, target, M, N, K, M, N, N, split, (long long)M * N);
+      done = true;
+    }
+  }
+  if (!done)
+    gemm_kernel<T, float, true, true, G::BM, G::BN, G::BK, 0><<<dim3(grid_tiles(M, N, G::BM, G::BN), 1, nz),
+                                                                kThreads, 0, st>>>(
+        a, b, nullptr, target, M, N, K, M, N, N, split, (long long)M * N);
+  if (nz > 1) {
+    const long long n4 = (long long)M * N / 4;
+    split_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(partial, c, n4, nz, (long long)M * N);
+  }
+  return hipGetLastError();
+}
+
+template hipError_t launch_gemm_nt<bf16>(const bf16*, const bf16*, bf16*, int, int, int, hipStream_t);
+template hipError_t launch_gemm_nt<float>(const float*, const float*, float*, int, int, int, hipStream_t);
+template hipError_t launch_gemm_tn<bf16>(const bf16*, const bf16*, float*, float*, int, int, int, int, hipStream_t);
+template hipError_t launch_gemm_tn<float>(const float*, const float*, float*, float*, int, int, int, int,
+                                          hipStream_t);
 template hipError_t launch_reconstruct<bf16>(const bf16*, const bf16*, bf16*, int, int, int, hipStream_t);
 template hipError_t launch_reconstruct<float>(const float*, const float*, float*, int, int, int, hipStream_t);
 template hipError_t launch_dc<bf16>(const bf16*, const bf16*, const bf16*, float*, float*, int, int, int, hipStream_t);

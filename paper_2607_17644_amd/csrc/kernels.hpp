@@ -32,6 +32,20 @@ template <typename T>
 hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float* partial, int M, int N, int K,
                      hipStream_t st);
 
+// Plain GEMMs of the output projection (Alg. 1 step 7) on the same kernels:
+//   gemm_nt: c[M][N] = a[M][K] @ w^T, w stored [N][K]; element-dtype output
+//   gemm_tn: c[M][N] = a^T @ b, a stored [K][M], b [K][N]; fp32 output, contraction split
+//            into nsplit ranges (partial: nsplit * M * N floats when nsplit > 1) summed in
+//            ascending order
+template <typename T>
+hipError_t launch_gemm_nt(const T* a, const T* w, T* c, int M, int N, int K, hipStream_t st);
+template <typename T>
+hipError_t launch_gemm_tn(const T* a, const T* b, float* c, float* partial, int M, int N, int K, int nsplit,
+                          hipStream_t st);
+// contraction splits gemm_tn is given for an M x N output over K (element size esize):
+// enough workgroups for the GPU, each split at least 512 indices; a function of the shape only
+int gemm_tn_splits(int M, int N, int K, int esize);
+
 struct AttnFwdArgs {
   const void* q;      // [B,S,H,DN+DR]
   const void* k_pe;   // [B,S,DR]
