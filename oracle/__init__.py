@@ -13,12 +13,15 @@ Modules:
   * ``producers`` — the per-token producers around the latent all-gather: the
                    latent RMS normalisation (Alg. 1 step 1) and the decoupled
                    rotary embedding of k_pe / q_rope, with their backward.
+  * ``out_proj`` — the consumer after the out all-to-all: the output projection
+                   W_o of Alg. 1 step 7 and its backward.
 
 Parity status: every function of ``laga`` is pinned by tests/test_oracle.py
 (brute force, absorbed form, finite differences, closed forms, invariants,
 causal prefix, torch SDPA), every one of ``producers`` by
 tests/test_producers_oracle.py (hand-computed rotations, closed forms, rotation
-algebra, finite differences). The paper prints no worked numeric example of the
+algebra, finite differences), and ``out_proj`` by tests/test_out_proj_oracle.py
+(scalar loops, finite differences, bilinear identities, special weights). The paper prints no worked numeric example of the
 attention outputs, so no pin compares against values printed in the paper.
 """
 from .laga import (reconstruct_kv, attn_fwd, attn_bwd, attn_fwd_rows,

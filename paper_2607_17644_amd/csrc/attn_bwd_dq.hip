@@ -184,17 +184,18 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
 // Every wave issues the same number of loads per stage (the K fill is rounded up to
 // whole rounds of the workgroup, and key blocks past a wave's queries load a dummy
 // block that is not read), so the ring waits can count loads exactly.
-template <int DN, int DR, int DV, int WPH, int NS>
+template <int DN, int DR, int DV, int WPH, int NS, int TPW>
 __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, KB = 32, NW = WPH;
   constexpr int KCPR = DQK / 8, NCPR = DN / 8, KP = KCPR + 4;  // pitch % 8 == 4
-  static_assert(KCPR % 4 == 0 && DQK % 32 == 0 && NS == 4, "192-wide K rows, four stages");
+  static_assert(KCPR % 4 == 0 && DQK % 32 == 0 && (NS == 3 || NS == 4), "192-wide K rows, 3 or 4 stages");
+  static_assert(TPW == 1 || TPW == 2, "one or two query tiles per wave");
   constexpr int KCH = (KB * KP + 64 * NW - 1) / (64 * NW) * (64 * NW);  // K chunks, whole rounds
-  constexpr int F = KCH / 64 / NW + 2;                                 // loads per wave per stage
+  constexpr int F = KCH / 64 / NW + 2 * TPW;                           // loads per wave per stage
+  constexpr int DSE = NW * TPW * KB * 32;                              // dS^T elements per stage
   __shared__ __attribute__((aligned(16))) T sK0[KCH * 8], sK1[KCH * 8], sK2[KCH * 8], sK3[KCH * 8];
-  __shared__ __attribute__((aligned(16))) T sD0[NW * KB * 32], sD1[NW * KB * 32], sD2[NW * KB * 32],
-      sD3[NW * KB * 32];
+  __shared__ __attribute__((aligned(16))) T sD0[DSE], sD1[DSE], sD2[DSE], sD3[DSE];
 
   const T* __restrict__ kpe = (const T*)P.k_pe;
   const T* __restrict__ kv = (const T*)P.kv;
@@ -208,25 +209,37 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
   const int b = bh / H, h = bh % H;
 
   const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
-  const int t = qblk * NW + wave;  // this wave's query tile
-  const bool wave_ok = t < TT;
-  const int nk = wave_ok ? ds_tile_keys(TT, P.causal, t) : 0;  // keys stored for the tile
-  const T* dtile = ds + (wave_ok ? ds_tile_offset(TT, P.causal, bh, t) : 0);
-  const int kend = P.causal ? min(S, (qblk + 1) * NW * 32) : S;
+  // this wave's query tiles t0 .. t0 + TPW - 1 (consecutive, so tile i sees 32 i more keys)
+  const int t0 = (qblk * NW + wave) * TPW;
+  int nk[TPW];
+  const T* dtile[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const bool ok = t0 + i < TT;
+    nk[i] = ok ? ds_tile_keys(TT, P.causal, t0 + i) : 0;  // keys stored for the tile
+    dtile[i] = ds + (ok ? ds_tile_offset(TT, P.causal, bh, t0 + i) : 0);
+  }
+  const int kend = P.causal ? min(S, (qblk + 1) * NW * TPW * 32) : S;
   const int ntiles = (kend + KB - 1) / KB;
 
-  f32x16 dqa[DQK / 32];
+  f32x16 dqa[TPW][DQK / 32];
 #pragma unroll
-  for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
+  for (int i = 0; i < TPW; ++i)
+#pragma unroll
+    for (int j = 0; j < DQK / 32; ++j) dqa[i][j] = f32x16{};
 
   auto fill = [&](T* dk, T* dd, int kt) {
     pad_fill_chunks<T, KB, KCPR, KP, NW, KCH>(dk, wave, l, [&](int r, int c) {
       const size_t row = (size_t)(b * S + min(kt + r, S - 1));
       return c < NCPR ? kv + (row * H + h) * DKVH + c * 8 : kpe + row * DR + (c - NCPR) * 8;
     });
-    const T* src = kt < nk ? dtile + (size_t)kt * 32 : dtile;  // dummy block when not stored
-    g2lds16(src + l * 8, dd + wave * KB * 32);
-    g2lds16(src + 512 + l * 8, dd + wave * KB * 32 + 512);
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const T* src = kt < nk[i] ? dtile[i] + (size_t)kt * 32 : dtile[i];  // dummy block when not stored
+      T* dst = dd + (wave * TPW + i) * KB * 32;
+      g2lds16(src + l * 8, dst);
+      g2lds16(src + 512 + l * 8, dst + 512);
+    }
   };
 
   for (int i = 0; i < NS - 1 && i < ntiles; ++i) {
@@ -234,6 +247,23 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
     else if (i == 1) fill(sK1, sD1, KB);
     else fill(sK2, sD2, 2 * KB);
   }
+  // one K fragment feeds the MFMAs of every tile of the wave that sees the key block
+  auto product = [&](const T* tk, const T* td, auto first) {
+    constexpr int I0 = decltype(first)::value;  // tiles before I0 do not see this block
+#pragma unroll
+    for (int kk = 0; kk < KB / 16; ++kk) {
+      const int ra = kk * 16 + 4 * g;
+      bf16x8 zf[TPW];
+#pragma unroll
+      for (int i = I0; i < TPW; ++i) zf[i] = pad_tr_frag<4>(td + i * KB * 32, ra, ra + 8, 0);
+#pragma unroll
+      for (int db = 0; db < DQK / 32; ++db) {
+        const bf16x8 kf = pad_tr_frag<KP>(tk, ra, ra + 8, db * 32);
+#pragma unroll
+        for (int i = I0; i < TPW; ++i) mma(dqa[i][db], kf, zf[i]);
+      }
+    }
+  };
   auto step = [&](auto stage, int it) {
     constexpr int ST = decltype(stage)::value;
     const int kt = it * KB;
@@ -245,38 +275,36 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
       T* nd_ = NX == 0 ? sD0 : NX == 1 ? sD1 : NX == 2 ? sD2 : sD3;
       fill(nk_, nd_, kt + (NS - 1) * KB);
     }
-    if (kt < nk) {  // wave-uniform: key blocks past the tile's queries hold no dS
-      const T* tk = ST == 0 ? sK0 : ST == 1 ? sK1 : ST == 2 ? sK2 : sK3;
-      const T* td = (ST == 0 ? sD0 : ST == 1 ? sD1 : ST == 2 ? sD2 : sD3) + wave * KB * 32;
-#pragma unroll
-      for (int kk = 0; kk < KB / 16; ++kk) {
-        const int ra = kk * 16 + 4 * g;
-        const bf16x8 zf = pad_tr_frag<4>(td, ra, ra + 8, 0);
-#pragma unroll
-        for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], pad_tr_frag<KP>(tk, ra, ra + 8, db * 32), zf);
-      }
-    }
+    const T* tk = ST == 0 ? sK0 : ST == 1 ? sK1 : ST == 2 ? sK2 : sK3;
+    const T* td = (ST == 0 ? sD0 : ST == 1 ? sD1 : ST == 2 ? sD2 : sD3) + wave * TPW * KB * 32;
+    // wave-uniform: key blocks past a tile's queries hold no dS for it; nk[i] grows with i
+    if (kt < nk[0]) product(tk, td, std::integral_constant<int, 0>{});
+    else if (TPW > 1 && kt < nk[TPW - 1]) product(tk, td, std::integral_constant<int, TPW - 1>{});
   };
   for (int it = 0; it < ntiles; it += NS) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
     if (it + 2 < ntiles) step(std::integral_constant<int, 2>{}, it + 2);
-    if (it + 3 < ntiles) step(std::integral_constant<int, 3>{}, it + 3);
+    if constexpr (NS == 4)
+      if (it + 3 < ntiles) step(std::integral_constant<int, NS - 1>{}, it + 3);
   }
 
   // accumulator column n holds the query stored at position n of the dS^T rows
-  const int my_q = t * 32 + ds_query_of_position(n);
-  if (!wave_ok || my_q >= S) return;
-  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll
-  for (int db = 0; db < DQK / 32; ++db)
+  for (int i = 0; i < TPW; ++i) {
+    const int my_q = (t0 + i) * 32 + ds_query_of_position(n);
+    if (t0 + i >= TT || my_q >= S) continue;
+    T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      bf16x4 v;
+    for (int db = 0; db < DQK / 32; ++db)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
-      *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
-    }
+      for (int rr = 0; rr < 4; ++rr) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[i][db][4 * rr + e] * P.scale);
+        *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
+      }
+  }
 }
 
 // dQ from the stored dS^T with K/V rebuilt on chip (kv_mode FUSED; bf16, 192/128-wide
@@ -394,6 +422,15 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
 
 }  // namespace
 
+// dq_ds_kernel's shape: 8 waves (two per SIMD, which hides the latency of the dS^T
+// stream) with one 32-query tile each. Measured at S=16384, H=16: 0.97 ms; 4 waves with
+// two tiles each (one K fragment read feeds two MFMAs) 1.37 ms, 4 waves with one 1.63 ms.
+#ifndef DQ_WAVES
+#define DQ_WAVES 8
+#define DQ_TPW 1
+#define DQ_NS 4
+#endif
+
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   using Tl = BwdTiles<T>;
@@ -401,10 +438,15 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   P.n_blocks = (P.S + BR - 1) / BR;
   if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
     if (P.ds) {
-      constexpr int WPH = 8;
-      P.n_blocks = (P.ds_T + WPH - 1) / WPH;
-      if (P.w_t) dq_ds_fused_kernel<DN, DR, DV><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
-      else dq_ds_kernel<DN, DR, DV, WPH, 4><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
+      if (P.w_t) {
+        constexpr int WPH = 8;
+        P.n_blocks = (P.ds_T + WPH - 1) / WPH;
+        dq_ds_fused_kernel<DN, DR, DV><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
+      } else {
+        // DQ_WAVES waves x DQ_TPW query tiles of 32 per workgroup
+        P.n_blocks = (P.ds_T + DQ_WAVES * DQ_TPW - 1) / (DQ_WAVES * DQ_TPW);
+        dq_ds_kernel<DN, DR, DV, DQ_WAVES, DQ_NS, DQ_TPW><<<dim3(P.n_blocks * P.H, B), 64 * DQ_WAVES, 0, st>>>(P);
+      }
       return hipGetLastError();
     }
   }

@@ -71,17 +71,18 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
 
   f32x16 sacc[BC / 32];
 #pragma unroll
-  for (int kb = 0; kb < BC / 32; ++kb) {
+  for (int kb = 0; kb < BC / 32; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) {
+  for (int ks = 0; ks < DQK / 16; ++ks)
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb) {
       const frag_t<T> a = ks < DN / 16
           ? lds_frag<T>(sKh + (kb * 32 + n) * PK + ks * 16 + 8 * g)
           : lds_frag<T>(sP + (kb * 32 + n) * PP + (ks - DN / 16) * 16 + 8 * g);
       mma(sacc[kb], a, qf[ks]);
     }
-  }
 
   // mask (only tiles crossing the diagonal or the end), running max on the raw scores
   // (scale > 0), p = exp2(s * scale_log2 - m) as one FMA + v_exp_f32, O rescaled only
@@ -132,9 +133,9 @@ __device__ __forceinline__ void fwd_tile(const T* sKh, int PK, const T* sP, int 
 #pragma unroll
   for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
 #pragma unroll
-  for (int db = 0; db < DV / 32; ++db)
+  for (int kk = 0; kk < BC / 16; ++kk)
 #pragma unroll
-    for (int kk = 0; kk < BC / 16; ++kk) {
+    for (int db = 0; db < DV / 32; ++db) {
       const int ra = kk * 16 + 4 * g;
       const frag_t<T> a = TrRead<T>::get(sVh, PV, ra, ra + 8, db * 32);
       mma(oacc[db], a, pf[kk]);
@@ -414,10 +415,13 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
     frag_t<T> pf[BC / 16];
 #pragma unroll
     for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
+    // key chunks outer, value blocks inner: consecutive MFMAs accumulate into different
+    // blocks of O^T, so none waits for the result of the one issued just before it (each
+    // block still sums its key chunks in ascending order)
 #pragma unroll
-    for (int db = 0; db < DV / 32; ++db)
+    for (int kk = 0; kk < BC / 16; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < BC / 16; ++kk) {
+      for (int db = 0; db < DV / 32; ++db) {
         const int ra = kk * 16 + 4 * g;
         mma(oacc[db], swz_tr_frag<VCPR>(tv, ra, ra + 8, db * 32), pf[kk]);
       }

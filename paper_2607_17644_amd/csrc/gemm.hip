@@ -162,10 +162,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
         frag_t<T> fa2[WM];
 #pragma unroll
         for (int i = 0; i < WM; ++i) fa2[i] = TA::frag(sA2, (wm * WM + i) * 32, ks);
+        // all hi products, then all lo ones (per accumulator the same order; see gemm_big_kernel)
 #pragma unroll
         for (int j = 0; j < WN; ++j)
 #pragma unroll
-          for (int i = 0; i < WM; ++i) { mma(acc[j][i], fb[j], fa[i]); mma(acc[j][i], fb[j], fa2[i]); }
+          for (int i = 0; i < WM; ++i) mma(acc[j][i], fb[j], fa[i]);
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int i = 0; i < WM; ++i) mma(acc[j][i], fb[j], fa2[i]);
       } else {
         frag_t<T> fb2[WN];
 #pragma unroll
@@ -173,7 +178,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
 #pragma unroll
         for (int j = 0; j < WN; ++j)
 #pragma unroll
-          for (int i = 0; i < WM; ++i) { mma(acc[j][i], fb[j], fa[i]); mma(acc[j][i], fb2[j], fa[i]); }
+          for (int i = 0; i < WM; ++i) mma(acc[j][i], fb[j], fa[i]);
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int i = 0; i < WM; ++i) mma(acc[j][i], fb2[j], fa[i]);
       }
     }
     __syncthreads();
@@ -353,15 +362,23 @@ __global__ __launch_bounds__(256, 1) void gemm_big_kernel(
       if (SPLIT) fX[ks][j] = rx.get(st + TA + TB, xsel, ks, j);
     }
   };
-  auto mmas = [&](int ks, int j0, int j1) {  // n blocks [j0, j1) of step ks
+  // n blocks [j0, j1) of step ks. With a low-half operand every accumulator takes the hi
+  // product before the lo one as before, but all hi products of the call are issued first:
+  // an MFMA that accumulates onto the one just issued waits for its result, so back-to-back
+  // hi, lo pairs on one accumulator would run the matrix unit at half rate.
+  auto mmas = [&](int ks, int j0, int j1) {
 #pragma unroll
     for (int j = j0; j < j1; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        mma(acc[j][i], fB[ks][j], fA[ks][i]);
-        if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
-        if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
-      }
+      for (int i = 0; i < 4; ++i) mma(acc[j][i], fB[ks][j], fA[ks][i]);
+    if (SPLIT)
+#pragma unroll
+      for (int j = j0; j < j1; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
+          if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
+        }
   };
 
   const int npre = min(NSLOT, nst);
