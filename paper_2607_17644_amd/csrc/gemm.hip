@@ -12,6 +12,10 @@
 // C^T = B^T A^T block by block, which puts 4 consecutive output columns in each
 // lane's accumulators for vectorised stores.
 //
+// The reconstruct (a 512-long contraction writing 256 bytes per output row and head)
+// runs as a persistent variant of the large-tile kernel that spreads each tile's
+// stores over the next tile's MFMAs (gemm_stream_kernel).
+//
 // Per output element the contraction runs over K in ascending 16-wide steps
 // (one MFMA each) with fp32 accumulation; tile shapes and the dW token split do
 // not depend on N, so a column of the output is bit-identical whatever N (the
@@ -441,6 +445,218 @@ __global__ __launch_bounds__(256, 1) void gemm_big_kernel(
     }
 }
 
+// ------------------------------------------------------------------ streamed large tiles (bf16 out)
+// The 4-wave 256 x 256 tile of gemm_big_kernel (no split, bf16 output) for a short
+// contraction such as the latent's 512, where the 256 x 256 x 2-byte results of a tile
+// take as long to write as its MFMAs take to compute, and a workgroup per tile writes
+// them all at once while every other CU does the same. Here a persistent workgroup
+// takes tiles q = blockIdx.x, + gridDim.x, ... and one LDS ring runs through all of
+// them (the next tile's first stages are copied while the current one finishes). A
+// finished tile's accumulators are rounded to bf16 and paired across the two
+// half-waves (v_permlane32_swap: 8 consecutive columns per lane) into 32 16-byte
+// stores per wave, and those stores are issued two per stage over the first 16 stages
+// of the next tile, so the writes run at an even rate behind the MFMAs. Per output
+// element the products are accumulated in the same order as in gemm_big_kernel: the
+// results are bitwise equal.
+//
+// Stores and copies share the in-order vmcnt counter: the stores issued in the last
+// three stages are younger than the copies a stage waits for (those were issued three
+// stages back) and older than none of them, so the ring's wait allows exactly that
+// many more operations in flight.
+constexpr int kStreamStoreStages = 16;  // stages over which a tile's stores are spread
+
+template <int BM, int BN, bool A_KS, bool B_KS>
+__global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restrict__ A, const bf16* __restrict__ B,
+                                                             bf16* __restrict__ C, int M, int N, int K, int lda,
+                                                             int ldb, int ldc) {
+  static_assert(BM * BN == 4 * 128 * 128 && BM % 128 == 0 && BN % 128 == 0, "four 128 x 128 waves");
+  constexpr int WM = BM / 128;
+  constexpr int NSLOT = 4;
+  constexpr int TA = BM * kGK, TB = BN * kGK, STAGE = TA + TB;
+  __shared__ __attribute__((aligned(16))) bf16 sm[NSLOT * STAGE];
+  typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
+  const int n_tiles = N / BN, n_items = n_tiles * (M / BM);
+  const int G = gridDim.x, nst = K / kGK;                    // nst >= kStreamStoreStages
+  const int mine = (n_items - 1 - (int)blockIdx.x) / G + 1;  // tiles of this workgroup
+  const int total = mine * nst;                              // stages of this workgroup
+
+  const int l = threadIdx.x & 63, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;
+  const int wm = wave % WM, wn = wave / WM;
+
+  GFill<A_KS, BM> fa;
+  GFill<B_KS, BN> fb;
+  fa.init(wave, l, lda, 0, BM);  // offsets within a tile; the tile origin goes into the base
+  fb.init(wave, l, ldb, 0, BN);
+  auto tile_at = [&](int it, int& m0, int& n0) {
+    const int lin = xcd_remap((int)blockIdx.x + it * G, n_items);
+    n0 = (lin % n_tiles) * BN;
+    m0 = (lin / n_tiles) * BM;
+  };
+  int f_loc = 0, f_it = 0, f_m0, f_n0;  // the next stage to copy
+  tile_at(0, f_m0, f_n0);
+  auto fill_next = [&](int slot) {
+    const int k = f_loc * kGK;
+    bf16* st = sm + slot * STAGE;
+    fa.fill(A_KS ? A + (size_t)k * lda + f_m0 : A + (size_t)f_m0 * lda + k, st, wave);
+    fb.fill(B_KS ? B + (size_t)k * ldb + f_n0 : B + (size_t)f_n0 * ldb + k, st + TA, wave);
+    if (++f_loc == nst) {
+      f_loc = 0;
+      if (++f_it < mine) {
+        tile_at(f_it, f_m0, f_n0);
+      } else {  // past the last stage: copy it again into slots nobody reads any more
+        f_it = mine - 1;
+        f_loc = nst - 1;
+      }
+    }
+  };
+  constexpr int F = GFill<A_KS, BM>::PER + GFill<B_KS, BN>::PER;  // copies per wave and stage
+  constexpr int Y = 6;  // stores younger than the copies a stage waits for, in steady state
+  static_assert(3 * F + Y + 2 < 64, "vmcnt range");
+
+  GRead<A_KS, BM> ra;
+  GRead<B_KS, BN> rb;
+  ra.init(l, wm);
+  rb.init(l, wn);
+
+  f32x16 acc[4][4];
+  bf16x8 fA[2][4], fB[2][4];
+  u32x4 pay[16][2];  // the previous tile's results, block (j, i) = 4 j + i, as stored
+  auto read = [&](int slot, int ks) {
+    const bf16* st = sm + slot * STAGE;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      fA[ks][j] = ra.get(st, wm, ks, j);
+      fB[ks][j] = rb.get(st + TA, wn, ks, j);
+    }
+  };
+  auto mmas = [&](int ks, int j0, int j1) {
+#pragma unroll
+    for (int j = j0; j < j1; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mma(acc[j][i], fB[ks][j], fA[ks][i]);
+  };
+  // Results of block (j, i) as two 16-byte stores per lane: lane half g takes columns
+  // 16 p + 8 g .. + 7 (p = 0, 1) of its row; within a lane the 16 accumulators are 4
+  // runs (rr) of 4 consecutive columns at 8 rr + 4 g, so runs 2p and 2p + 1 are
+  // exchanged with the other half-wave.
+  auto pack = [&](int j, int i, u32x4 (&out)[2]) {
+    uint32_t x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+      const bf16x2 v = {(bf16)acc[j][i][2 * e], (bf16)acc[j][i][2 * e + 1]};
+      x[e] = __builtin_bit_cast(uint32_t, v);
+    }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const auto r = __builtin_amdgcn_permlane32_swap(x[4 * p], x[4 * p + 2], false, false);
+      const auto s = __builtin_amdgcn_permlane32_swap(x[4 * p + 1], x[4 * p + 3], false, false);
+      out[p] = u32x4{r[0], s[0], r[1], s[1]};
+    }
+  };
+  auto store = [&](const u32x4 (&v)[2], int m0, int n0, int b) {
+    const int j = b >> 2, i = b & 3;
+    bf16* row = C + (size_t)(m0 + 128 * wm + 32 * i + (l & 31)) * ldc + n0 + 128 * wn + 32 * j + 8 * g;
+    *reinterpret_cast<u32x4*>(row) = v[0];
+    *reinterpret_cast<u32x4*>(row + 16) = v[1];
+  };
+
+  constexpr int RPS = (A_KS ? 8 : 4) + (B_KS ? 8 : 4);  // LDS reads per step
+  constexpr int DS_READ = 0x100, MFMA = 0x008;
+  // First half of stage t: step-1 reads interleaved with the step-0 MFMAs (which
+  // restart every accumulator from zero in the first stage of a tile), then half of
+  // the step-1 MFMAs.
+  auto head = [&](int t, bool first) {
+    read(t % NSLOT, 1);
+    if (first) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[j][i] = f32x16{};
+          mma(acc[j][i], fB[0][j], fA[0][i]);
+        }
+    } else {
+      mmas(0, 0, 4);
+    }
+    mmas(1, 0, 2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 4, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, 4, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(MFMA, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Second half of stage t: wait for stage t + 1, barrier, refill the slot of stage t,
+  // read the step-0 operands of stage t + 1 with the other half of the step-1 MFMAs.
+  // Every stage refills a slot (past the end with copies of the last stage), so two
+  // stages of copies are always in flight behind the awaited one. With EXACT the wait
+  // also leaves the Y stores of the last three stages in flight (they are younger than
+  // the copies of stage t + 1, issued three stages back); otherwise it waits for them.
+  // (s_waitcnt takes its count as an immediate: a count chosen at run time costs taken
+  // branches every stage, which leave the matrix unit idle.)
+  auto tail = [&](int t, auto exact) {
+    if (decltype(exact)::value) wait_vmem_le<2 * F + Y>();
+    else wait_vmem_le<2 * F>();
+    lds_barrier();
+    fill_next(t % NSLOT);
+    __builtin_amdgcn_sched_barrier(0);
+    read((t + 1) % NSLOT, 0);  // (after the last stage: a harmless read of a stale slot)
+    mmas(1, 2, 4);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 2, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, 4, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int t = 0; t < NSLOT; ++t) fill_next(t);  // (total >= kStreamStoreStages > NSLOT)
+  wait_vmem_le<(NSLOT - 1) * F>();
+  lds_barrier();
+  read(0, 0);
+
+  int c_m0 = 0, c_n0 = 0;  // the tile being accumulated
+  int e_m0 = 0, e_n0 = 0;  // the tile whose results are being stored
+  int t = 0;
+  // the first kStreamStoreStages stages of tile it, storing the previous tile's results
+  auto first_stages = [&](int it, auto exact) {
+#pragma unroll
+    for (int s = 0; s < kStreamStoreStages; ++s, ++t) {
+      head(t, s == 0);
+      if (it > 0) store(pay[s], e_m0, e_n0, s);
+      tail(t, exact);
+    }
+  };
+  for (int it = 0; it < mine; ++it) {
+    tile_at(it, c_m0, c_n0);
+    // From the third tile on (and with exactly kStreamStoreStages stages per tile) every
+    // stage has stores of its own and of the two stages before it in flight.
+    if (it >= 2 && nst == kStreamStoreStages) first_stages(it, std::true_type{});
+    else first_stages(it, std::false_type{});
+    for (int s = kStreamStoreStages; s < nst; ++s, ++t) {
+      head(t, false);
+      tail(t, std::false_type{});
+    }
+#pragma unroll
+    for (int b = 0; b < 16; ++b) pack(b >> 2, b & 3, pay[b]);
+    e_m0 = c_m0;
+    e_n0 = c_n0;
+  }
+#pragma unroll
+  for (int b = 0; b < 16; ++b) store(pay[b], e_m0, e_n0, b);
+  wait_vmem();  // the surplus copies land before the workgroup's LDS is released
+}
+
+// The streamed kernel applies to whole tiles and at least kStreamStoreStages stages per tile.
+bool gemm_stream_ok(int M, int N, int K, size_t a_elems, size_t b_elems) {
+  return M % 256 == 0 && N % 256 == 0 && K % kGK == 0 && K / kGK >= kStreamStoreStages && 2 * a_elems < (1ull << 32) &&
+         2 * b_elems < (1ull << 32);
+}
+
 // The large-tile kernel applies to bf16 operands whose contraction range splits into
 // multiples of 32, with M and N multiples of 8, and whose byte offsets within an
 // operand fit the 32-bit offsets of the copies.
@@ -467,6 +683,7 @@ template <> struct GemmCfg<bf16> { static constexpr int BM = 128, BN = 128, BK =
 template <> struct GemmCfg<float> { static constexpr int BM = 64, BN = 64, BK = 16; };
 
 inline int grid_tiles(int M, int N, int BM, int BN) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
+constexpr int kCUs = 256;  // compute units of the gfx950 part (one streamed workgroup each)
 
 }  // namespace
 
@@ -474,6 +691,12 @@ template <typename T>
 hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K, hipStream_t st) {
   using G = GemmCfg<T>;
   if constexpr (sizeof(T) == 2) {
+    if (gemm_stream_ok(M, N, K, (size_t)M * K, (size_t)K * N)) {
+      const int tiles = grid_tiles(M, N, 256, 256);
+      gemm_stream_kernel<256, 256, false, true><<<tiles < kCUs ? tiles : kCUs, 256, 0, st>>>(
+          c, w, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N);
+      return hipGetLastError();
+    }
     if (gemm_big_ok(M, N, K, K, (size_t)M * K, (size_t)K * N)) {
       gemm_big_kernel<256, 256, false, true, 0, bf16><<<grid_tiles(M, N, 256, 256), 256, 0, st>>>(
           c, w, nullptr, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N, /*k_chunk=*/K, 0);
