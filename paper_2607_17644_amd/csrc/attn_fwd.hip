@@ -19,6 +19,9 @@
 // with log2(e) folded into the scale; lse is returned in natural log.
 #include <type_traits>
 
+// direct global->LDS copies issued as inline assembly: LDS reads then get exact waits
+// (every ring here orders its copies with an explicit vmcnt wait and a barrier)
+#define LAGA_LDS_DMA_ASM 1
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -359,15 +362,29 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
     const T* tp = ST == 0 ? sP0 : sP1;
     const T* tv = (ST == 0 ? sV0 : sV1) + hh * BC * DV;
 
-    f32x16 sacc[BC / 32];
+    // S^T = K Q^T: product i takes contraction step ks = i / KB of key block kb = i % KB
+    // (consecutive products go to different accumulators); its K fragment is read from
+    // LDS PF products ahead into a ring of PF + 1 registers (the order of the reads and
+    // products is pinned, so the compiler cannot trade the prefetch for registers).
+    constexpr int KB = BC / 32, NSP = KB * (DQK / 16), PF = 3;
+    auto k_frag = [&](int i) {
+      const int ks = i / KB, kb = i % KB;
+      return ks < DN / 16 ? swz_frag<T, KCPR>(tk, kb * 32 + n, 2 * ks + g)
+                          : swz_frag<T, PCPR>(tp, kb * 32 + n, 2 * (ks - DN / 16) + g);
+    };
+    f32x16 sacc[KB];
+    {
+      frag_t<T> ab[PF + 1];
 #pragma unroll
-    for (int kb = 0; kb < BC / 32; ++kb) {
-      sacc[kb] = f32x16{};
+      for (int i = 0; i < PF; ++i) ab[i] = k_frag(i);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ks = 0; ks < DQK / 16; ++ks) {
-        const frag_t<T> a = ks < DN / 16 ? swz_frag<T, KCPR>(tk, kb * 32 + n, 2 * ks + g)
-                                         : swz_frag<T, PCPR>(tp, kb * 32 + n, 2 * (ks - DN / 16) + g);
-        mma(sacc[kb], a, qf[ks]);
+      for (int i = 0; i < NSP; ++i) {
+        if (i + PF < NSP) ab[(i + PF) % (PF + 1)] = k_frag(i + PF);
+        const int ks = i / KB, kb = i % KB;
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[i % (PF + 1)], qf[ks], ks == 0 ? f32x16{} : sacc[kb],
+                                                          0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
@@ -417,14 +434,24 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
     for (int kk = 0; kk < BC / 16; ++kk) pf[kk] = acc_to_frag<T>(sacc[kk >> 1], kk & 1);
     // key chunks outer, value blocks inner: consecutive MFMAs accumulate into different
     // blocks of O^T, so none waits for the result of the one issued just before it (each
-    // block still sums its key chunks in ascending order)
+    // block still sums its key chunks in ascending order); V fragments prefetched as K's
+    constexpr int NDB = DV / 32, NPV = (BC / 16) * NDB;
+    auto v_frag = [&](int i) {
+      const int kk = i / NDB, db = i % NDB, ra = kk * 16 + 4 * g;
+      return swz_tr_frag<VCPR>(tv, ra, ra + 8, db * 32);
+    };
+    {
+      frag_t<T> vb[PF + 1];
 #pragma unroll
-    for (int kk = 0; kk < BC / 16; ++kk)
+      for (int i = 0; i < PF; ++i) vb[i] = v_frag(i);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int db = 0; db < DV / 32; ++db) {
-        const int ra = kk * 16 + 4 * g;
-        mma(oacc[db], swz_tr_frag<VCPR>(tv, ra, ra + 8, db * 32), pf[kk]);
+      for (int i = 0; i < NPV; ++i) {
+        if (i + PF < NPV) vb[(i + PF) % (PF + 1)] = v_frag(i + PF);
+        mma(oacc[i % NDB], vb[i % (PF + 1)], pf[i / NDB]);
+        __builtin_amdgcn_sched_barrier(0);
       }
+    }
   };
   for (int it = 0; it < ntiles; it += 2) {
     step(std::integral_constant<int, 0>{}, it);
