@@ -567,11 +567,14 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
         __builtin_nontemporal_store(zf[kk], reinterpret_cast<bf16x8*>(dsr + kk * 8));
     }
   };
+  // Every tile step refills a slot, past the end with another copy of the last tile (a
+  // slot nobody reads any more), so one tile of copies is always in flight behind the
+  // awaited one and the wait needs no branch.
+  auto tile_q = [&](int j) { return qt_begin + min(j, ntiles - 1) * BQ; };
   auto sync = [&](int j) {
-    if (j + 1 < ntiles) wait_vmem_le<F>();
-    else wait_vmem();
+    wait_vmem_le<F>();
     lds_barrier();
-    if (j + 2 < ntiles) fill((j + 2) % NS, qt_begin + (j + 2) * BQ);
+    fill((j + 2) % NS, tile_q(j + 2));
   };
 
   // The sweep over the query tiles, compiled twice: with HILO the rope band of dK^T takes
@@ -579,7 +582,7 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   auto sweep = [&](auto hc) {
   constexpr bool HILO = decltype(hc)::value;
   fill(0, qt_begin);
-  if (ntiles > 1) fill(1, qt_begin + BQ);
+  fill(1, tile_q(1));
   f32x16 sa0, dp0, sa1, dp1;
   bf16x8 pf[2], zf[2], zl[2];
   sync(0);
@@ -693,6 +696,7 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
   };
   if (kb == 0) sweep(std::true_type{});
   else sweep(std::false_type{});
+  wait_vmem();  // the surplus copies land before the workgroup's LDS is released
 
   if (!key_ok) return;
   const size_t row = krow * H + h;

@@ -242,11 +242,12 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
     }
   };
 
-  for (int i = 0; i < NS - 1 && i < ntiles; ++i) {
-    if (i == 0) fill(sK0, sD0, 0);
-    else if (i == 1) fill(sK1, sD1, KB);
-    else fill(sK2, sD2, 2 * KB);
-  }
+  // Every step refills a stage, past the last block with in-bounds dummies (clamped K
+  // rows, the tile's first dS block) that nobody reads, so NS - 2 stages of loads are
+  // always in flight behind the awaited one and the waits need no branch.
+  fill(sK0, sD0, 0);
+  fill(sK1, sD1, KB);
+  if constexpr (NS == 4) fill(sK2, sD2, 2 * KB);
   // one K fragment feeds the MFMAs of every tile of the wave that sees the key block
   auto product = [&](const T* tk, const T* td, auto first) {
     constexpr int I0 = decltype(first)::value;  // tiles before I0 do not see this block
@@ -267,9 +268,9 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
   auto step = [&](auto stage, int it) {
     constexpr int ST = decltype(stage)::value;
     const int kt = it * KB;
-    ring_wait<NS, F>(min(NS - 2, ntiles - 1 - it));  // this wave's loads of block `it` have landed
+    wait_vmem_le<(NS - 2) * F>();  // this wave's loads of block `it` have landed
     __syncthreads();  // ... and everyone's; the stage filled next (read last at it - 1) is free
-    if (it + NS - 1 < ntiles) {
+    {
       constexpr int NX = (ST + NS - 1) % NS;
       T* nk_ = NX == 0 ? sK0 : NX == 1 ? sK1 : NX == 2 ? sK2 : sK3;
       T* nd_ = NX == 0 ? sD0 : NX == 1 ? sD1 : NX == 2 ? sD2 : sD3;
@@ -289,6 +290,7 @@ __global__ __launch_bounds__(64 * WPH, 1) void dq_ds_kernel(BwdParams P) {
       if (it + 3 < ntiles) step(std::integral_constant<int, NS - 1>{}, it + 3);
   }
 
+  wait_vmem();  // the surplus loads land before the workgroup's LDS is released
   // accumulator column n holds the query stored at position n of the dS^T rows
 #pragma unroll
   for (int i = 0; i < TPW; ++i) {
