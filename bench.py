@@ -36,6 +36,11 @@ PEAK_HBM_GBS = 8000.0
 WORKLOAD = "v3_train_s16384"
 
 
+def progress(msg):
+    """One line per finished section on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -268,13 +273,16 @@ def gpu_bench(w, steps, warmup, clock_probe_s=0.0, graph=False, extras=True):
 
     main = StepRunner(w)
     res = main.time(steps, warmup)
+    progress(f"timed steps done: {res['ms']['step']:.4f} ms per step")
     res["graph_ms_per_step"] = graph_step_ms(main.step, steps) if graph else None
     res["workspace_bytes"] = main.ws_bytes
     if not extras:
         return res
     res["prologue"] = prologue_bench(w, main.p, steps, warmup)
+    progress("producers done")
     if clock_probe_s > 0:
         res["clock"] = clock_under_load(main.step, clock_probe_s)
+        progress("clock probe done")
     out_m, lse_m = main.out.clone(), main.lse.clone()
     dq_m = main.dq.clone()
     grads_m = [t.clone() for t in (main.dc, main.dkpe, main.dw)]
@@ -289,6 +297,7 @@ def gpu_bench(w, steps, warmup, clock_probe_s=0.0, graph=False, extras=True):
                            "dq_max_abs_vs_store": float((rec.dq.float() - dq_m.float()).abs().max()),
                            "other_grads_bitwise_equal": all(torch.equal(a, b) for a, b in
                                                             zip((rec.dc, rec.dkpe, rec.dw), grads_m))}
+    progress("dq-recompute step done")
     del rec
     torch.cuda.empty_cache()
 
@@ -300,6 +309,7 @@ def gpu_bench(w, steps, warmup, clock_probe_s=0.0, graph=False, extras=True):
                                                                    torch.equal(fu.lse, lse_m)),
                     "grads_bitwise_equal_materialised": bool(torch.equal(fu.dq, dq_m) and all(
                         torch.equal(a, b) for a, b in zip((fu.dc, fu.dkpe, fu.dw), grads_m)))}
+    progress("fused K/V step done")
     del fu
     torch.cuda.empty_cache()
     return res
@@ -569,6 +579,7 @@ def main():
     cpu = None
     if not a.no_cpu_baseline:
         cpu = cpu_baseline(w, a.cpu_heads)
+        progress("CPU oracle sample done")
     rd = lambda dct: {k: round(v, 4) for k, v in dct.items()}
     line = {
         "metric": f"attention-block TFLOP/s and ms/step (fwd+bwd), S={S}, {H} heads, % bf16 MFMA peak",
@@ -612,9 +623,11 @@ def main():
                          "grads_bitwise_equal_materialised": r["grads_bitwise_equal_materialised"]}
     if not a.no_extras and a.seq_len is None:
         line["sweep"] = sweep_bench(w, (2048, 4096, 8192), a.steps, a.warmup)
+        progress("S sweep done")
     line["prologue_outside_step"] = g.get("prologue")
     if not a.no_extras and a.seq_len is None and a.heads is None:
         line["out_proj_outside_step"] = out_proj_bench(w, a.steps, a.warmup)
+        progress("W_o done")
     line["clock_under_load"] = g.get("clock")
     line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
