@@ -37,6 +37,17 @@ def test_bf16(S, H):
     assert np.all(np.abs(got - ref) <= ulp + 1e-5)
 
 
+# whole 256 x 256 tiles: the persistent kernel, with 1 (4096 x 16), 2 (8192 x 16), 2-3
+# uneven (9984 x 16: 624 tiles over 256 workgroups), 3, 4 (the benchmark shape) and 8
+# (16384 x 32) tiles per workgroup
+@pytest.mark.parametrize("S,H", [(8192, 16), (9984, 16), (12288, 16), (16384, 16), (16384, 32)])
+def test_bf16_persistent(S, H):
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=S, n_heads=H)
+    got, ref, _, _ = run(w)
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+    assert np.all(np.abs(got - ref) <= ulp + 1e-5)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_head_slices_bitwise(dtype):
     """kv columns of a 16-head shard are bit-identical to the same columns of the 128-head run."""
