@@ -172,6 +172,186 @@ __global__ __launch_bounds__(64 * WPH) void dq_kernel(BwdParams P) {
 }
 
 
+// dQ recomputed without any S x S buffer (bf16, 192/128-wide heads): the forward's
+// structure with dP and dS added. A workgroup of 8 waves owns 256 queries of one head (a
+// wave 32, lane <-> query); 64-key tiles of K = [K_nope || k_pe] and V stream through a
+// two-stage LDS ring of direct global->LDS loads into XOR-swizzled tiles. Per 32-key
+// block: S^T = K Q^T and dP^T = V dO^T (A = K / V rows from LDS, B = the wave's Q and dO
+// in registers, fragments read three products ahead), P^T = exp2(S^T scale_log2 - lse2),
+// dS^T = P^T (dP^T - delta) in the accumulators' lanes, then dQ^T += K^T dS^T with K^T
+// from transposing LDS reads and dS^T straight from the accumulators. The arithmetic
+// per element is the key-stationary pass's (S and dP on the same MFMA products, the
+// same exp2 argument, dS rounded once to bf16) and dQ sums the keys in ascending
+// 16-wide steps, as the pass over the stored dS^T does: dq is bitwise equal to it.
+template <int DN, int DR, int DV, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void dq_rec_kernel(BwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, BC = 64, BR = 32 * NW;
+  constexpr int KCPR = DN / 8, PCPR = DR / 8, VCPR = DV / 8;
+  constexpr int NKS = DQK / 16, NVS = DV / 16, NDB = DQK / 32, NDN = DN / 32;
+  static_assert(KCPR == 16 && PCPR == 8 && VCPR == 16, "swizzles are defined for 128/64/128-wide rows");
+  // two ring stages as distinct LDS objects (compile-time stage offsets in the reads)
+  __shared__ __attribute__((aligned(16))) T sK0[BC * DN], sK1[BC * DN];
+  __shared__ __attribute__((aligned(16))) T sP0[BC * DR], sP1[BC * DR];
+  __shared__ __attribute__((aligned(16))) T sV0[BC * DV], sV1[BC * DV];
+
+  const T* __restrict__ q = (const T*)P.q;
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ kv = (const T*)P.kv;
+  const T* __restrict__ dout = (const T*)P.dout;
+  const int S = P.S, H = P.H;
+
+  const int total = P.n_blocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;  // heavy first
+  const int bh = lin / P.n_blocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q0 = qblk * BR + wave * 32;
+  const int my_q = q0 + n;
+  const int kend = P.causal ? min(S, (qblk + 1) * BR) : S;
+
+  frag_t<T> qf[NKS], of[NVS];
+  float lse2 = 0.f, dlt = 0.f;
+  {
+    const bool ok = my_q < S;
+    const size_t base = (size_t)(b * S + (ok ? my_q : 0)) * H + h;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      qf[ks] = *reinterpret_cast<const frag_t<T>*>(q + base * DQK + ks * 16 + 8 * g);
+      if (!ok) qf[ks] = frag_t<T>{};
+    }
+#pragma unroll
+    for (int ks = 0; ks < NVS; ++ks) {
+      of[ks] = *reinterpret_cast<const frag_t<T>*>(dout + base * DV + ks * 16 + 8 * g);
+      if (!ok) of[ks] = frag_t<T>{};
+    }
+    if (ok) {
+      lse2 = P.lse2[(size_t)(b * H + h) * P.S_pad + my_q];
+      dlt = P.delta[(size_t)(b * H + h) * P.S_pad + my_q];
+    }
+  }
+  f32x16 dqa[NDB];
+#pragma unroll
+  for (int i = 0; i < NDB; ++i) dqa[i] = f32x16{};
+
+  // key rows past S are clamped to S - 1 (valid memory) and masked below
+  SwzRowFill<T, BC, KCPR, NW> kfill, vfill;
+  SwzRowFill<T, BC, PCPR, NW> pfill;
+  kfill.init(wave, l, H * DKVH);
+  vfill.init(wave, l, H * DKVH);
+  pfill.init(wave, l, DR);
+  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
+    const T* kvb = kv + ((size_t)(b * S + kt) * H + h) * DKVH;
+    kfill.fill(dk, wave, l, kvb, H * DKVH, S - kt);
+    vfill.fill(dv, wave, l, kvb + DN, H * DKVH, S - kt);
+    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, S - kt);
+  };
+
+  constexpr int PF = 3;
+  const int ntiles = (kend + BC - 1) / BC;
+  fill(sK0, sP0, sV0, 0);
+  auto step = [&](auto stage, int it) {
+    constexpr int ST = decltype(stage)::value;
+    const int kt = it * BC;
+    wait_vmem();      // this wave's loads of tile `it` have landed
+    __syncthreads();  // ... and everyone's; the other stage is free
+    if (it + 1 < ntiles) {
+      if constexpr (ST == 0) fill(sK1, sP1, sV1, kt + BC);
+      else fill(sK0, sP0, sV0, kt + BC);
+    }
+    if (P.causal && kt > q0 + 31) return;  // wave-uniform: every key of the tile is masked
+    const T* tk = ST == 0 ? sK0 : sK1;
+    const T* tp = ST == 0 ? sP0 : sP1;
+    const T* tv = ST == 0 ? sV0 : sV1;
+    const bool need_mask = (P.causal && kt + BC - 1 > q0) || (kt + BC > S);
+#pragma unroll
+    for (int kb = 0; kb < BC / 32; ++kb) {
+      // product i of S^T (even i < 16 and i >= 16: contraction step a_ks(i) of K) and of
+      // dP^T (odd i < 16: step i / 2 of V), alternating accumulators
+      auto a_is_s = [](int i) { return i >= 16 || (i & 1) == 0; };
+      auto a_ks = [](int i) { return i >= 16 ? 8 + (i - 16) : i >> 1; };
+      auto a_frag = [&](int i) {
+        const int ks = a_ks(i), row = kb * 32 + n;
+        if (!a_is_s(i)) return swz_frag<T, VCPR>(tv, row, 2 * ks + g);
+        return ks < DN / 16 ? swz_frag<T, KCPR>(tk, row, 2 * ks + g)
+                            : swz_frag<T, PCPR>(tp, row, 2 * (ks - DN / 16) + g);
+      };
+      constexpr int NA = NKS + NVS;  // 20 products
+      f32x16 sa, dp;
+      {
+        frag_t<T> ab[PF + 1];
+#pragma unroll
+        for (int i = 0; i < PF; ++i) ab[i] = a_frag(i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+          if (i + PF < NA) ab[(i + PF) % (PF + 1)] = a_frag(i + PF);
+          if (a_is_s(i))
+            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[i % (PF + 1)], qf[a_ks(i)], i == 0 ? f32x16{} : sa,
+                                                         0, 0, 0);
+          else
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[i % (PF + 1)], of[a_ks(i)], i == 1 ? f32x16{} : dp,
+                                                         0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      if (need_mask) {
+        asm volatile("");  // a kept branch: only tiles on the diagonal or at the end
+        // live keys: accumulator row (r/4)*8 + r%4 of key block kb < klim - kt - 32 kb - 4 g
+        const int lim = (P.causal ? min(S, my_q + 1) : S) - kt - 32 * kb - 4 * g;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sa[r] = (r >> 2) * 8 + (r & 3) < lim ? sa[r] : -INFINITY;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(__builtin_fmaf(sa[r], P.scale_log2, -lse2));
+        dp[r] = p * (dp[r] - dlt);
+      }
+      bf16x8 zf[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) zf[kk] = acc_to_frag<T>(dp, kk);
+      // dQ^T += K^T dS^T: product i = 16-key chunk kk = i / NDB, dQ block db = i % NDB
+      auto k_tr = [&](int i) {
+        const int kk = i / NDB, db = i % NDB, ra = kb * 32 + kk * 16 + 4 * g;
+        return db < NDN ? swz_tr_frag<KCPR>(tk, ra, ra + 8, db * 32)
+                        : swz_tr_frag<PCPR>(tp, ra, ra + 8, (db - NDN) * 32);
+      };
+      constexpr int NQ = 2 * NDB;  // 12 products
+      {
+        frag_t<T> kb_[PF + 1];
+#pragma unroll
+        for (int i = 0; i < PF; ++i) kb_[i] = k_tr(i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) {
+          if (i + PF < NQ) kb_[(i + PF) % (PF + 1)] = k_tr(i + PF);
+          mma(dqa[i % NDB], kb_[i % (PF + 1)], zf[i / NDB]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+  }
+
+  if (my_q >= S) return;
+  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      bf16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
+      *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
+    }
+}
+
 // dQ from the stored dS^T (bf16, 192/128-wide heads): the key-stationary pass leaves
 // dS^T = P * (dP - delta) of every causal (query tile, key) pair in the workspace, so
 // this pass is a streaming product dQ^T (192 x 32 per wave) += K^T dS^T over the
@@ -432,6 +612,13 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
 #define DQ_TPW 1
 #define DQ_NS 4
 #endif
+// dq_rec_kernel's shape: 4 waves (one per SIMD, 128 queries per workgroup). Measured at
+// S=16384, H=16: 2.16-2.38 ms; 8 waves need more than their 256 registers (98 spilled):
+// 7.8 ms. Interleaving one key block's dS arithmetic with the other's MFMAs in a pinned
+// order measured 2 % slower than the plain order.
+#ifndef DQ_REC_WAVES
+#define DQ_REC_WAVES 4
+#endif
 
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
@@ -451,6 +638,13 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
       }
       return hipGetLastError();
     }
+  }
+  if constexpr (sizeof(T) == 2 && DN == 128 && DR == 64 && DV == 128) {
+    // no dS^T store: recompute S, P, dP and dS per key tile
+    constexpr int RW = DQ_REC_WAVES;
+    P.n_blocks = (P.S + 32 * RW - 1) / (32 * RW);
+    dq_rec_kernel<DN, DR, DV, RW><<<dim3(P.n_blocks * P.H, B), 64 * RW, 0, st>>>(P);
+    return hipGetLastError();
   }
   dq_kernel<T, DN, DR, DV, Tl::BC, Tl::WPH_Q><<<dim3(P.n_blocks * P.H, B), 64 * Tl::WPH_Q, 0, st>>>(P);
   return hipGetLastError();
