@@ -109,8 +109,9 @@ typedef enum { LAGA_OP_FWD = 0, LAGA_OP_BWD = 1, LAGA_OP_PROLOGUE_BWD = 2 } laga
  *        recompute (below) whatever this field says.
  * RECOMPUTE: no buffer of S*S size anywhere (workspace linear in S): the dq pass is
  *        query-stationary and recomputes the scores and dP for its queries, which costs
- *        the Q K^T and dO V^T products a second time. Results equal FROM_STORE's up to
- *        fp32 summation order (dq) or exactly (every other output). */
+ *        the Q K^T and dO V^T products a second time. Every output equals FROM_STORE's
+ *        exactly for bf16 with 192/128-wide heads (the same products, exp2 arguments,
+ *        roundings and key order); elsewhere dq may differ in fp32 summation order. */
 typedef enum { LAGA_DQ_FROM_STORE = 0, LAGA_DQ_RECOMPUTE = 1 } laga_dq_mode_t;
 
 typedef struct {

@@ -237,8 +237,9 @@ def test_s16384_two_heads_against_the_full_oracle():
                                           (257, 3, 2, True)])
 def test_recompute_mode_against_the_oracle(S, H, B, causal):
     """dq_mode RECOMPUTE (no S x S buffer): the full oracle comparison, and every gradient
-    but dq bit-identical to the dS^T-store mode (the key-stationary pass is the same
-    arithmetic without the store; dq comes from a pass that recomputes the scores)."""
+    bit-identical to the dS^T-store mode (the key-stationary pass is the same arithmetic
+    without the store; the recomputing dq pass forms the same dS values and sums them in
+    the same key order as the pass over the store)."""
     import torch
     import paper_2607_17644_amd as L
     w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal)
@@ -246,7 +247,7 @@ def test_recompute_mode_against_the_oracle(S, H, B, causal):
     d = dev_inputs(w, x)
     g_store, _, _ = gpu_step(w, d)
     g, _, _ = gpu_step(w, d, dq_mode=L.DQ_RECOMPUTE)
-    for k in ("dc_kv", "dk_pe", "dw_kv_b"):
+    for k in ("dq", "dc_kv", "dk_pe", "dw_kv_b"):
         assert torch.equal(g[k], g_store[k]), k
     ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
     for k in NAMES:
@@ -270,7 +271,7 @@ def test_recompute_mode_s16384():
     d = dev_inputs(w, x)
     g_store, _, _ = gpu_step(w, d)
     g, _, _ = gpu_step(w, d, dq_mode=L.DQ_RECOMPUTE)
-    for k in ("dc_kv", "dk_pe", "dw_kv_b"):
+    for k in ("dq", "dc_kv", "dk_pe", "dw_kv_b"):
         assert torch.equal(g[k], g_store[k]), k
     S = w.seq_len
     rows = [0, 1, 100, 5000, S - 1]
@@ -280,10 +281,6 @@ def test_recompute_mode_s16384():
     tail = S - 128
     rb = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], row_start=tail, **okw(w))
     check_tol("dq", f64(g["dq"][:, tail:]), rb["dq"][:, tail:], "bf16", "recompute tail")
-    # both dq passes compute the same sums in different fp32 orders
-    diff = (g["dq"].float() - g_store["dq"].float()).abs().max().item()
-    print(f"recompute vs store dq max |diff| {diff:.3e}")
-    assert diff < 2e-2
 
 
 def test_s16384_sixteen_heads_against_the_full_oracle():
