@@ -602,6 +602,140 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
     }
 }
 
+// The same product with the K_nope rebuild organised around its operand traffic (d_c =
+// 512): 4 waves (one per SIMD, 128 queries per workgroup); wave w owns K_nope column
+// block w and keeps its 32 rows of W_h^T (pi-ordered, 32 fragments) in registers for the
+// whole kernel; per 64-key step the latent rows are copied once into LDS (direct loads,
+// one 1 KB row per wave instruction, rows padded to 65 chunks: conflict-free row
+// fragments) and each wave rebuilds its column block for both 32-key halves (two
+// independent accumulator chains), so W_h^T is read once per workgroup and each latent
+// row once per step instead of once per wave and step. Operand roles, contraction
+// order and rounding are those of dq_ds_fused_kernel: the K tile and dq are the same bit
+// for bit.
+template <int DN, int DR, int DV, int DC>
+__global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
+  using T = bf16;
+  constexpr int DQK = DN + DR, DKVH = DN + DV, NW = 4, KB = 64, NKS = DC / 16;
+  constexpr int KP = DQK / 8 + 4;  // K tile pitch in 16-byte chunks (% 8 == 4: transposing reads)
+  constexpr int CP = DC / 8 + 1;   // latent row pitch in chunks (odd: row fragments conflict-free)
+  static_assert(DN == NW * 32 && DR == 64 && DC == 64 * 8, "one 32-column K_nope block per wave; a latent row per copy");
+  __shared__ __attribute__((aligned(16))) T sC[KB * CP * 8];
+  __shared__ __attribute__((aligned(16))) T sK[KB * KP * 8];
+  __shared__ __attribute__((aligned(16))) T sD[NW * 2 * 32 * 32];
+
+  const T* __restrict__ kpe = (const T*)P.k_pe;
+  const T* __restrict__ ds = (const T*)P.ds;
+  const int S = P.S, H = P.H, TT = P.ds_T;
+
+  const int total = P.n_blocks * H * gridDim.y;
+  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
+  const int qblk = P.n_blocks - 1 - lin % P.n_blocks;  // heavy first
+  const int bh = lin / P.n_blocks;
+  const int b = bh / H, h = bh % H;
+
+  const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);
+  const int t = qblk * NW + wave;  // this wave's query tile
+  const bool wave_ok = t < TT;
+  const int nk = wave_ok ? ds_tile_keys(TT, P.causal, t) : 0;
+  const T* dtile = ds + (wave_ok ? ds_tile_offset(TT, P.causal, bh, t) : 0);
+  const int kend = P.causal ? min(S, (qblk + 1) * NW * 32) : S;
+  const int nsteps = (kend + KB - 1) / KB;
+
+  // W_h^T rows of this wave's column block in the order pi (bits 2 and 3 swapped), so
+  // that lane (n, g) of the rebuild accumulator holds columns 16 hh + 8 g + e
+  const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
+  frag_t<T> wf[NKS];
+  {
+    const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + wave * 32 + pi_n) * DC + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) wf[ks] = *reinterpret_cast<const frag_t<T>*>(wt + ks * 16);
+  }
+  const T* cg = (const T*)P.c_kv + (size_t)b * S * DC;
+
+  f32x16 dqa[DQK / 32];
+#pragma unroll
+  for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
+
+  constexpr int PF = 3;
+  for (int st = 0; st < nsteps; ++st) {
+    const int kt = st * KB;
+    __syncthreads();  // the previous step's reads of sC / sK / sD are done
+    // latent rows kt .. kt + 63 (rows past S clamped: their dS is zero), wave w rows 16 w ..
+#pragma unroll
+    for (int i = 0; i < KB / NW; ++i) {
+      const int r = wave * (KB / NW) + i;
+      g2lds16(cg + (size_t)min(kt + r, S - 1) * DC + l * 8, sC + r * CP * 8);
+    }
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {  // this wave's dS^T blocks of the step (a dummy when not stored)
+      const int kb = kt + 32 * sub;
+      const T* src = kb < nk ? dtile + (size_t)kb * 32 : dtile;
+      g2lds16(src + l * 8, sD + (wave * 2 + sub) * 1024);
+      g2lds16(src + 512 + l * 8, sD + (wave * 2 + sub) * 1024 + 512);
+    }
+#pragma unroll
+    for (int i = 0; i < KB * DR / 8 / (64 * NW); ++i) {  // k_pe rows
+      const int c = tid + i * 64 * NW, r = c / (DR / 8), ch = c % (DR / 8);
+      const int key = min(kt + r, S - 1);
+      const chunk16 v = *reinterpret_cast<const chunk16*>(kpe + (size_t)(b * S + key) * DR + ch * 8);
+      *reinterpret_cast<chunk16*>(sK + r * KP * 8 + DN + ch * 8) = v;
+    }
+    wait_vmem();
+    __syncthreads();
+    {  // K_nope column block `wave` for keys kt .. kt + 63: two chains, one per 32-key half
+      auto c_frag = [&](int i) {  // product i: contraction step i / 2 of key half i % 2
+        return *reinterpret_cast<const frag_t<T>*>(sC + (32 * (i & 1) + n) * CP * 8 + (i >> 1) * 16 + 8 * g);
+      };
+      f32x16 acc[2] = {f32x16{}, f32x16{}};
+      frag_t<T> cb[PF + 1];
+#pragma unroll
+      for (int i = 0; i < PF; ++i) cb[i] = c_frag(i);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 2 * NKS; ++i) {
+        if (i + PF < 2 * NKS) cb[(i + PF) % (PF + 1)] = c_frag(i + PF);
+        mma(acc[i & 1], wf[i >> 1], cb[i % (PF + 1)]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh) {
+        T* dst = sK + (32 * kh + n) * KP * 8 + wave * 32 + 8 * g;
+        *reinterpret_cast<bf16x8*>(dst) = acc_to_frag<T>(acc[kh], 0);
+        *reinterpret_cast<bf16x8*>(dst + 16) = acc_to_frag<T>(acc[kh], 1);
+      }
+    }
+    __syncthreads();  // the whole K tile is in LDS
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      if (kt + 32 * sub < nk) {  // wave-uniform: key blocks past the tile's queries hold no dS
+        const T* tk = sK + 32 * sub * KP * 8;
+        const T* td = sD + (wave * 2 + sub) * 1024;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int ra = kk * 16 + 4 * g;
+          const bf16x8 zf = pad_tr_frag<4>(td, ra, ra + 8, 0);
+#pragma unroll
+          for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], pad_tr_frag<KP>(tk, ra, ra + 8, db * 32), zf);
+        }
+      }
+    }
+  }
+
+  const int my_q = t * 32 + ds_query_of_position(n);
+  if (!wave_ok || my_q >= S) return;
+  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
+#pragma unroll
+  for (int db = 0; db < DQK / 32; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      bf16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
+      *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
+    }
+}
+
 }  // namespace
 
 // dq_ds_kernel's shape: 8 waves (two per SIMD, which hides the latency of the dS^T
@@ -627,7 +761,10 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   P.n_blocks = (P.S + BR - 1) / BR;
   if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
     if (P.ds) {
-      if (P.w_t) {
+      if (P.w_t && P.d_c == kFusedMaxDc) {
+        P.n_blocks = (P.ds_T + 3) / 4;
+        dq_ds_fused2_kernel<DN, DR, DV, kFusedMaxDc><<<dim3(P.n_blocks * P.H, B), 256, 0, st>>>(P);
+      } else if (P.w_t) {
         constexpr int WPH = 8;
         P.n_blocks = (P.ds_T + WPH - 1) / WPH;
         dq_ds_fused_kernel<DN, DR, DV><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
