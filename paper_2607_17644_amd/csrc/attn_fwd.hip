@@ -517,7 +517,8 @@ __device__ __forceinline__ void load_latent_rows(const T* __restrict__ cg, T* sC
   }
 }
 
-template <typename T, int DN, int DR, int DV, int BC, int WPH, int DCMAX>
+// DCF: d_c as a compile-time constant (0: the run-time P.d_c, up to DCMAX)
+template <typename T, int DN, int DR, int DV, int BC, int WPH, int DCMAX, int DCF>
 __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams P) {
   constexpr int DQK = DN + DR, DKVH = DN + DV, E = Elems16<T>::n, NT = 64 * WPH, NW = WPH;
   constexpr int PK = DN + 8, PP = DR + 8, PV = DV + 32 / (int)sizeof(T), PC = DCMAX + 8;
@@ -611,16 +612,37 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
       const T* wrow[NCB];
 #pragma unroll
       for (int i = 0; i < NCB; ++i) wrow[i] = wt + (size_t)(h * DKVH + (cb0 + i) * 32 + n) * dc + 8 * g;
-      for (int ks = 0; ks < dc / 16; ++ks) {
-        frag_t<T> a[NCB], bb[NKB];
+      if constexpr (DCF > 0 && NCB == 1) {
+        // d_c known at compile time: the W^T fragments stream from L2 through a ring of
+        // WR registers, WR contraction steps ahead of their MFMAs (one load in flight per
+        // step would leave every step waiting for L2)
+        constexpr int NKS = DCF / 16, WR = 16;
+        static_assert(NKS >= WR, "ring shorter than the contraction");
+        frag_t<T> ar[WR];
 #pragma unroll
-        for (int i = 0; i < NCB; ++i) a[i] = *reinterpret_cast<const frag_t<T>*>(wrow[i] + ks * 16);
+        for (int u = 0; u < WR; ++u) ar[u] = *reinterpret_cast<const frag_t<T>*>(wrow[0] + u * 16);
 #pragma unroll
-        for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
+        for (int ks = 0; ks < NKS; ++ks) {
+          const frag_t<T> a = ar[ks % WR];
+          if (ks + WR < NKS) ar[ks % WR] = *reinterpret_cast<const frag_t<T>*>(wrow[0] + (ks + WR) * 16);
+          frag_t<T> bb[NKB];
 #pragma unroll
-        for (int i = 0; i < NCB; ++i)
+          for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
 #pragma unroll
-          for (int j = 0; j < NKB; ++j) mma(acc[i][j], a[i], bb[j]);
+          for (int j = 0; j < NKB; ++j) mma(acc[0][j], a, bb[j]);
+        }
+      } else {
+        for (int ks = 0; ks < dc / 16; ++ks) {
+          frag_t<T> a[NCB], bb[NKB];
+#pragma unroll
+          for (int i = 0; i < NCB; ++i) a[i] = *reinterpret_cast<const frag_t<T>*>(wrow[i] + ks * 16);
+#pragma unroll
+          for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
+#pragma unroll
+          for (int i = 0; i < NCB; ++i)
+#pragma unroll
+            for (int j = 0; j < NKB; ++j) mma(acc[i][j], a[i], bb[j]);
+        }
       }
 #pragma unroll
       for (int i = 0; i < NCB; ++i)
@@ -740,7 +762,10 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
   P.scale_log2 = a.scale * 1.4426950408889634f;
   P.causal = a.causal;
   dim3 grid(P.n_qblocks * a.H, a.B, 1);
-  attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, FW, kFusedMaxDc><<<grid, 64 * FW, 0, st>>>(P);
+  if (a.d_c == kFusedMaxDc)
+    attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, FW, kFusedMaxDc, kFusedMaxDc><<<grid, 64 * FW, 0, st>>>(P);
+  else
+    attn_fwd_fused_kernel<T, DN, DR, DV, Tl::BC, FW, kFusedMaxDc, 0><<<grid, 64 * FW, 0, st>>>(P);
   return hipGetLastError();
 }
 
