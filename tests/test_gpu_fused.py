@@ -38,6 +38,14 @@ def test_fused_equals_materialised_bitwise(name, S, H, B, causal):
     assert scaled_err(f64(of), ro) < TOL[w.dtype] and scaled_err(f64(lf), rl) < TOL[w.dtype]
 
 
+def test_fused_other_latent_width_bitwise():
+    """d_c = 256 (the fused forward with a run-time latent width) against the materialised path."""
+    import torch
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=300, n_heads=3, d_c=256)
+    _, om, lm, of, lf = both(w)
+    assert torch.equal(om, of) and torch.equal(lm, lf)
+
+
 def test_fused_s16384_bitwise():
     """The full-size comparison configuration (S=16384, 16 heads): both paths agree exactly."""
     import torch
@@ -59,12 +67,13 @@ def test_fused_workspace_and_limits():
     assert e.value.status == 3
 
 
-@pytest.mark.parametrize("name,S,H,B,causal,dq_mode", [
-    ("tiny_fp32", 45, 4, 2, False, 0), ("tiny_fp32", 100, 4, 1, True, 0),
-    ("v3_shard_s4096", 300, 3, 2, True, 0), ("v3_shard_s4096", 2048, 16, 1, True, 0),
-    ("v3_shard_s4096", 65, 2, 1, False, 0), ("v3_shard_s4096", 1, 1, 1, True, 0),
-    ("v3_shard_s4096", 333, 2, 1, True, 1)])
-def test_fused_backward_equals_materialised_bitwise(name, S, H, B, causal, dq_mode):
+# d_c = 256: the kernels for a latent width other than the V3 512 (run-time d_c)
+@pytest.mark.parametrize("name,S,H,B,causal,dq_mode,d_c", [
+    ("tiny_fp32", 45, 4, 2, False, 0, None), ("tiny_fp32", 100, 4, 1, True, 0, None),
+    ("v3_shard_s4096", 300, 3, 2, True, 0, None), ("v3_shard_s4096", 2048, 16, 1, True, 0, None),
+    ("v3_shard_s4096", 65, 2, 1, False, 0, None), ("v3_shard_s4096", 1, 1, 1, True, 0, None),
+    ("v3_shard_s4096", 333, 2, 1, True, 1, None), ("v3_shard_s4096", 300, 3, 1, True, 0, 256)])
+def test_fused_backward_equals_materialised_bitwise(name, S, H, B, causal, dq_mode, d_c):
     """The backward in the fused mode (kv NULL) returns the materialised mode's gradients bit
     for bit, and they meet the oracle. bf16 with 192/128-wide heads rebuilds every K/V tile
     on chip (the key-stationary pass once per key, the dQ pass per query block) and writes
@@ -73,6 +82,8 @@ def test_fused_backward_equals_materialised_bitwise(name, S, H, B, causal, dq_mo
     import torch
     import paper_2607_17644_amd as L
     w = LI.WORKLOADS[name].replace(seq_len=S, n_heads=H, batch=B, causal=causal)
+    if d_c is not None:
+        w = w.replace(d_c=d_c)
     x = LI.make_inputs(w)
     d = dev_inputs(w, x)
     p = problem_for(w, dq_mode=dq_mode)
