@@ -24,6 +24,9 @@
 //                  the 32x32x16 MFMA, software-pipelined (see there); unless dq is
 //                  to be recomputed, it also stores dS^T for the dQ pass
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
+// and in attn_bwd_dq.hip, for bf16 with 192/128-wide heads: dq_ds_kernel (dQ as a
+// product over the stored dS^T), dq_rec_kernel (dQ recomputed, no S x S buffer) and
+// the fused-mode dQ kernels that rebuild K from the latent.
 #include <type_traits>
 
 // direct global->LDS copies issued as inline assembly (exact LDS-read waits; the
