@@ -49,9 +49,11 @@
  *     before any rounding to the element dtype.
  *   - Causal means key j is visible to query i iff j <= i (0-based positions in
  *     the gathered sequence, S_q == S_k). Non-causal attends to every key.
- *   - Supported head dims: (d_nope, d_rope, d_v) = (128, 64, 128) — DeepSeek-V3 —
- *     and (32, 16, 32); d_c a multiple of 32 up to 1024; S >= 1; B >= 1; H >= 1.
- *     Anything else returns LAGA_ERR_UNSUPPORTED.
+ *   - Supported head dims: (d_nope, d_rope, d_v) = (128, 64, 128) — DeepSeek-V3 —,
+ *     (64, 32, 64) and (32, 16, 32); d_c a multiple of 32 up to 1024; S >= 1;
+ *     B >= 1; H >= 1. Anything else returns LAGA_ERR_UNSUPPORTED. Each width is a
+ *     compile-time kernel instance (the tile shapes follow from it); the
+ *     DeepSeek-V3 widths have the tuned bf16 kernels, the others the generic ones.
  *   - Kernels index inside a tensor with 32-bit element offsets: B*S*H*W, with
  *     W = d_nope + max(d_rope, d_v) + max(d_nope, d_v), B*S*d_c, B*S, and
  *     16*d_c*H*(d_nope + d_v) must each stay below 2^31, else

@@ -23,6 +23,7 @@ struct Dims {
 
 bool is_v3(const laga_problem_t* p) { return p->d_nope == 128 && p->d_rope == 64 && p->d_v == 128; }
 bool is_small(const laga_problem_t* p) { return p->d_nope == 32 && p->d_rope == 16 && p->d_v == 32; }
+bool is_half(const laga_problem_t* p) { return p->d_nope == 64 && p->d_rope == 32 && p->d_v == 64; }
 
 laga_status_t validate(const laga_problem_t* p, Dims* d) {
   if (!p) return LAGA_ERR_NULL;
@@ -35,7 +36,7 @@ laga_status_t validate(const laga_problem_t* p, Dims* d) {
     return LAGA_ERR_UNSUPPORTED;
   if (p->dtype != LAGA_DTYPE_BF16 && p->dtype != LAGA_DTYPE_FP32) return LAGA_ERR_UNSUPPORTED;
   if (p->kv_mode != LAGA_KV_MATERIALIZED && p->kv_mode != LAGA_KV_FUSED) return LAGA_ERR_UNSUPPORTED;
-  if (!is_v3(p) && !is_small(p)) return LAGA_ERR_UNSUPPORTED;
+  if (!is_v3(p) && !is_small(p) && !is_half(p)) return LAGA_ERR_UNSUPPORTED;
   if (p->d_c % 32 != 0 || p->d_c > 1024) return LAGA_ERR_UNSUPPORTED;
   const int64_t tok = p->batch * p->seq_len;
   const int64_t wide = p->n_heads * (p->d_nope + (p->d_rope > p->d_v ? p->d_rope : p->d_v) +
@@ -344,10 +345,14 @@ laga_status_t laga_attn_fwd(const laga_problem_t* p, const void* q, const void* 
     if (is_v3(p))
       return from_hip(bf ? launch_attn_fwd_fused<bf16, 128, 64, 128>(a, workspace, st)
                          : launch_attn_fwd_fused<float, 128, 64, 128>(a, workspace, st));
+    if (is_half(p))
+      return from_hip(bf ? launch_attn_fwd_fused<bf16, 64, 32, 64>(a, workspace, st)
+                         : launch_attn_fwd_fused<float, 64, 32, 64>(a, workspace, st));
     return from_hip(bf ? launch_attn_fwd_fused<bf16, 32, 16, 32>(a, workspace, st)
                        : launch_attn_fwd_fused<float, 32, 16, 32>(a, workspace, st));
   }
   if (is_v3(p)) return from_hip(bf ? launch_attn_fwd<bf16, 128, 64, 128>(a, st) : launch_attn_fwd<float, 128, 64, 128>(a, st));
+  if (is_half(p)) return from_hip(bf ? launch_attn_fwd<bf16, 64, 32, 64>(a, st) : launch_attn_fwd<float, 64, 32, 64>(a, st));
   return from_hip(bf ? launch_attn_fwd<bf16, 32, 16, 32>(a, st) : launch_attn_fwd<float, 32, 16, 32>(a, st));
 }
 
@@ -404,6 +409,8 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
   hipError_t e;
   const int kstage = stage == LAGA_BWD_PREPARE ? 0 : stage == LAGA_BWD_DKDV ? 1 : stage == LAGA_BWD_DQ ? 2 : 3;
   if (v3) e = bf ? launch_attn_bwd<bf16, 128, 64, 128>(a, kstage, st) : launch_attn_bwd<float, 128, 64, 128>(a, kstage, st);
+  else if (is_half(p))
+    e = bf ? launch_attn_bwd<bf16, 64, 32, 64>(a, kstage, st) : launch_attn_bwd<float, 64, 32, 64>(a, kstage, st);
   else e = bf ? launch_attn_bwd<bf16, 32, 16, 32>(a, kstage, st) : launch_attn_bwd<float, 32, 16, 32>(a, kstage, st);
   if (e != hipSuccess || stage != LAGA_BWD_FINISH) return from_hip(e);
 

@@ -798,5 +798,7 @@ LAGA_INST_BWD(bf16, 128, 64, 128)
 LAGA_INST_BWD(float, 128, 64, 128)
 LAGA_INST_BWD(bf16, 32, 16, 32)
 LAGA_INST_BWD(float, 32, 16, 32)
+LAGA_INST_BWD(bf16, 64, 32, 64)
+LAGA_INST_BWD(float, 64, 32, 64)
 
 }  // namespace laga

@@ -792,5 +792,7 @@ LAGA_INST_DQ(bf16, 128, 64, 128)
 LAGA_INST_DQ(float, 128, 64, 128)
 LAGA_INST_DQ(bf16, 32, 16, 32)
 LAGA_INST_DQ(float, 32, 16, 32)
+LAGA_INST_DQ(bf16, 64, 32, 64)
+LAGA_INST_DQ(float, 64, 32, 64)
 
 }  // namespace laga

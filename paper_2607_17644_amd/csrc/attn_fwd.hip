@@ -785,5 +785,7 @@ LAGA_INST_FWD(bf16, 128, 64, 128)
 LAGA_INST_FWD(float, 128, 64, 128)
 LAGA_INST_FWD(bf16, 32, 16, 32)
 LAGA_INST_FWD(float, 32, 16, 32)
+LAGA_INST_FWD(bf16, 64, 32, 64)
+LAGA_INST_FWD(float, 64, 32, 64)
 
 }  // namespace laga

@@ -728,7 +728,8 @@ int dc_split_count(int tokens, int d_c, int K) {
   const bool big = gemm_big_ok(tokens, d_c, K, kGK, (size_t)tokens * K, (size_t)d_c * K);
   const int tiles = big ? grid_tiles(tokens, d_c, dc_bm(d_c), 65536 / dc_bm(d_c))
                         : grid_tiles(tokens, d_c, GemmCfg<bf16>::BM, GemmCfg<bf16>::BN);
-  const int max_split = K / 256;  // at least one head (256 contraction indices) per split
+  // at least 256 contraction indices (one 192/128-wide head) per split, and one split
+  const int max_split = K >= 512 ? K / 256 : 1;
   // large tiles: one workgroup per CU (256) is enough; small tiles want two or more
   const int want = big ? 256 : kMinGemmBlocks;
   int n = (want + tiles - 1) / tiles;

@@ -55,6 +55,22 @@ def test_v3_fp32_mode():
     check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=300, n_heads=2, dtype="fp32"))
 
 
+# 64/32/64-wide heads with a 256-wide latent: the generic backward kernels at a third head
+# width, both element types, both dq modes
+@pytest.mark.parametrize("dtype,S,H,B,causal,dq_mode", [
+    ("bf16", 2048, 8, 1, True, 0), ("bf16", 257, 3, 2, True, 0), ("bf16", 300, 2, 1, False, 0),
+    ("bf16", 1, 1, 1, True, 0), ("bf16", 333, 2, 1, True, 1), ("fp32", 300, 2, 1, True, 0),
+    ("fp32", 45, 3, 2, False, 1)])
+def test_half_width_heads(dtype, S, H, B, causal, dq_mode):
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal, dtype=dtype,
+                                                d_c=256, d_nope=64, d_rope=32, d_v=64)
+    x = LI.make_inputs(w)
+    g, _, _ = gpu_step(w, dev_inputs(w, x), dq_mode=dq_mode)
+    ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+    for k in NAMES:
+        check_tol(k, f64(g[k]), ref[k], w.dtype)
+
+
 @pytest.mark.parametrize("S", [16384, 16001])
 def test_s16384_sampled(S):
     """Training step at the per-rank shard (S=16384, 16 heads), as the benchmark runs it,

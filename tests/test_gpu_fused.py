@@ -127,3 +127,31 @@ def test_fused_backward_s16384_bitwise():
     assert torch.equal(of, out) and torch.equal(lf, lse)
     for n, a, b in zip(("dq", "dc_kv", "dk_pe", "dw_kv_b"), gm, gf):
         assert torch.equal(a, b), n
+
+
+@pytest.mark.parametrize("dtype,S,H,B,causal", [("bf16", 1024, 8, 1, True), ("bf16", 300, 3, 2, False),
+                                                ("fp32", 100, 2, 1, True)])
+def test_fused_half_width_heads_bitwise(dtype, S, H, B, causal):
+    """64/32/64-wide heads with a 256-wide latent: the fused forward rebuilds K/V on chip
+    and equals the materialised forward bit for bit; the fused backward rebuilds kv once
+    into the workspace and returns the materialised gradients bit for bit."""
+    import torch
+    import paper_2607_17644_amd as L
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal, dtype=dtype,
+                                                d_c=256, d_nope=64, d_rope=32, d_v=64)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    p = problem_for(w)
+    kv = L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"])
+    out, lse = L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv)
+    gm = L.laga_attn_bwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"])
+    pf = problem_for(w, kv_mode=L.KV_FUSED)
+    of, lf = L.laga_attn_fwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"])
+    gf = L.laga_attn_bwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], None, of, lf, d["dout"])
+    torch.cuda.synchronize()
+    assert torch.equal(of, out) and torch.equal(lf, lse)
+    for n, a, b in zip(("dq", "dc_kv", "dk_pe", "dw_kv_b"), gm, gf):
+        assert torch.equal(a, b), n
+    ro, rl = O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], n_heads=H, d_nope=w.d_nope,
+                        d_v=w.d_v, scale=w.scale, causal=causal)
+    assert scaled_err(f64(of), ro) < TOL[w.dtype] and scaled_err(f64(lf), rl) < TOL[w.dtype]

@@ -48,6 +48,16 @@ def test_v3_fp32_mode():
     check_full(LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=333, n_heads=2, dtype="fp32"))
 
 
+# 64/32/64-wide heads (half the DeepSeek-V3 widths, with a 256-wide latent): the generic
+# kernels at a third head width, in both element types, causal and not, ragged and tiled
+@pytest.mark.parametrize("dtype,S,H,B,causal", [("bf16", 2048, 8, 1, True), ("bf16", 257, 3, 2, True),
+                                                ("bf16", 300, 2, 1, False), ("bf16", 1, 1, 1, True),
+                                                ("fp32", 333, 2, 1, True), ("fp32", 45, 3, 2, False)])
+def test_half_width_heads(dtype, S, H, B, causal):
+    check_full(LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=S, n_heads=H, batch=B, causal=causal, dtype=dtype,
+                                                     d_c=256, d_nope=64, d_rope=32, d_v=64))
+
+
 def test_s16384_sampled_rows():
     """Full-size shard (S=16384, 16 heads) in the launch configuration the benchmark times;
     the oracle computes a sample of query rows one by one."""

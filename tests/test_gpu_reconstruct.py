@@ -48,6 +48,15 @@ def test_bf16_persistent(S, H):
     assert np.all(np.abs(got - ref) <= ulp + 1e-5)
 
 
+# 64/32/64-wide heads over a 256-wide latent: 128 columns per head
+@pytest.mark.parametrize("dtype,S,H", [("bf16", 300, 3), ("bf16", 2048, 8), ("fp32", 100, 2)])
+def test_half_width_heads(dtype, S, H):
+    w = LI.WORKLOADS["v3_shard_s4096"].replace(seq_len=S, n_heads=H, dtype=dtype, d_c=256, d_nope=64,
+                                               d_rope=32, d_v=64)
+    got, ref, _, _ = run(w)
+    assert err(got, ref) < TOL[dtype]
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_head_slices_bitwise(dtype):
     """kv columns of a 16-head shard are bit-identical to the same columns of the 128-head run."""
