@@ -19,7 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblaga.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "prologue.hip"]
+SOURCES = ["api.hip", "gemm.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_dq.hip", "prologue.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -37,6 +37,7 @@ FLAGS = [
 EXTRA = {
     "attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "attn_bwd_kv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 

@@ -10,23 +10,21 @@
 //
 // Kernels (all deterministic: no floating-point atomics anywhere):
 //   delta_kernel   one thread per (token, head)
-//   dkdv_kernel    key-stationary: a workgroup owns 32*WPH keys of one head and
-//                  sweeps the query tiles at or after them; lane <-> key layout
-//                  (S = Q K^T with K in registers), so P and dZ feed the
-//                  dV^T += dO^T P and dK^T += Q^T dZ products directly from the
-//                  accumulators, with dO^T / Q^T read by transposing LDS reads
-//   dq_kernel      query-stationary: a workgroup owns 32*WPH queries of one
-//                  head and sweeps the key tiles up to the diagonal; lane <->
-//                  query layout (S^T = K Q^T), dQ^T += K^T dZ^T with K^T read by
-//                  transposing LDS reads; it recomputes S and dP (the price of
-//                  not accumulating dQ with atomics)
-//   dkdv32_kernel  the same for bf16 with 192/128-wide heads, 32 keys per wave on
-//                  the 32x32x16 MFMA, software-pipelined (see there); unless dq is
+//   dkdv32_kernel  key-stationary dK/dV for bf16 with 192/128-wide heads: a wave owns
+//                  32 keys of one head and sweeps the query tiles at or after them;
+//                  lane <-> key layout (S = Q K^T with K in registers), so P and dZ
+//                  feed dV^T += dO^T P and dK^T += Q^T dZ directly from the
+//                  accumulators, with dO^T / Q^T read by transposing LDS reads;
+//                  software-pipelined on the 32x32x16 MFMA (see there); unless dq is
 //                  to be recomputed, it also stores dS^T for the dQ pass
 //   dkpe_kernel    dk_pe = sum over heads (ascending) of the per-head k_pe parts
-// and in attn_bwd_dq.hip, for bf16 with 192/128-wide heads: dq_ds_kernel (dQ as a
-// product over the stored dS^T), dq_rec_kernel (dQ recomputed, no S x S buffer) and
-// the fused-mode dQ kernels that rebuild K from the latent.
+// in attn_bwd_kv.hip: dkdv_kernel, the same key-stationary pass for the other element
+// types and head widths; and in attn_bwd_dq.hip: dq_kernel (query-stationary: a
+// workgroup owns 32*WPH queries of one head and sweeps the key tiles up to the
+// diagonal, recomputing S and dP - the price of not accumulating dQ with atomics), and
+// for bf16 with 192/128-wide heads dq_ds_kernel (dQ as a product over the stored dS^T),
+// dq_rec_kernel (dQ recomputed, no S x S buffer) and the fused-mode dQ kernels that
+// rebuild K from the latent.
 #include <type_traits>
 
 // direct global->LDS copies issued as inline assembly (exact LDS-read waits; the
@@ -84,203 +82,6 @@ __global__ __launch_bounds__(256) void delta_kernel(const T* __restrict__ out, c
     }
   }
 }
-
-// ------------------------------------------------------------------ dK, dV
-template <typename T, int DN, int DR, int DV, int BQ, int WPH>
-__global__ __launch_bounds__(64 * WPH) void dkdv_kernel(BwdParams P) {
-  constexpr int DQK = DN + DR, DKVH = DN + DV, DQK32 = round32(DQK);
-  constexpr int NT = 64 * WPH, BK = 32 * WPH, E = Elems16<T>::n;
-  constexpr int PQ = lds_pitch<T>(DQK32), PO = lds_pitch<T>(DV);
-  constexpr int QCH = DQK / E, OCH = DV / E;                 // chunks per row
-  constexpr int TILE_CHUNKS = BQ * (QCH + OCH);
-  constexpr int PER_THREAD = (TILE_CHUNKS + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) T sQ[BQ * PQ];
-  __shared__ __attribute__((aligned(16))) T sO[BQ * PO];
-  __shared__ __attribute__((aligned(16))) float sL[BQ];
-  __shared__ __attribute__((aligned(16))) float sD[BQ];
-
-  const T* __restrict__ q = (const T*)P.q;
-  const T* __restrict__ kpe = (const T*)P.k_pe;
-  const T* __restrict__ kv = (const T*)P.kv;
-  const T* __restrict__ dout = (const T*)P.dout;
-  const int S = P.S, H = P.H;
-
-  const int total = P.n_blocks * H * gridDim.y;
-  const int lin = xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, total);
-  const int kb = lin % P.n_blocks;  // ascending: the first key blocks see the most queries
-  const int bh = lin / P.n_blocks;
-  const int b = bh / H, h = bh % H;
-
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, n = l & 31, g = l >> 5;
-  const int k0 = kb * BK + wave * 32;  // first key of this wave
-  const int my_k = k0 + n;
-
-  // zero the padding columns [DQK, DQK32) once: transposing reads of Q^T blocks touch them
-  if (DQK32 > DQK)
-    for (int i = tid; i < BQ * (DQK32 - DQK); i += NT)
-      sQ[(i / (DQK32 - DQK)) * PQ + DQK + i % (DQK32 - DQK)] = to_elem<T>(0.f);
-
-  // this lane's key and value rows (B operands of S = Q K^T and dP = dO V^T)
-  frag_t<T> kf[DQK / 16], vf[DV / 16];
-  {
-    const bool ok = my_k < S;
-    const size_t row = (size_t)(b * S + (ok ? my_k : 0));
-    const T* kvr = kv + (row * H + h) * DKVH;
-#pragma unroll
-    for (int ks = 0; ks < DQK / 16; ++ks) {
-      const T* src = ks < DN / 16 ? kvr + ks * 16 + 8 * g : kpe + row * DR + (ks - DN / 16) * 16 + 8 * g;
-      if (ok) kf[ks] = *reinterpret_cast<const frag_t<T>*>(src);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kf[ks][e] = to_elem<T>(0.f);
-    }
-#pragma unroll
-    for (int ks = 0; ks < DV / 16; ++ks) {
-      if (ok) vf[ks] = *reinterpret_cast<const frag_t<T>*>(kvr + DN + ks * 16 + 8 * g);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[ks][e] = to_elem<T>(0.f);
-    }
-  }
-
-  f32x16 dk[DQK32 / 32], dv[DV / 32];
-#pragma unroll
-  for (int i = 0; i < DQK32 / 32; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dk[i][r] = 0.f;
-#pragma unroll
-  for (int i = 0; i < DV / 32; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dv[i][r] = 0.f;
-
-  chunk16 stage[PER_THREAD];
-  float st_l = 0.f, st_d = 0.f;
-  auto load_tile = [&](int qt) {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * NT;
-      stage[i] = zero_chunk();
-      if (c < TILE_CHUNKS) {
-        const int row = c / (QCH + OCH), j = c % (QCH + OCH);
-        const int qi = qt + row;
-        if (qi < S) {
-          const size_t base = (size_t)(b * S + qi) * H + h;
-          stage[i] = j < QCH ? *reinterpret_cast<const chunk16*>(q + base * DQK + j * E)
-                             : *reinterpret_cast<const chunk16*>(dout + base * DV + (j - QCH) * E);
-        }
-      }
-    }
-    if (tid < BQ) {
-      const int qi = qt + tid;
-      st_l = qi < S ? P.lse2[(size_t)(b * H + h) * P.S_pad + qi] : 0.f;
-      st_d = qi < S ? P.delta[(size_t)(b * H + h) * P.S_pad + qi] : 0.f;
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * NT;
-      if (c < TILE_CHUNKS) {
-        const int row = c / (QCH + OCH), j = c % (QCH + OCH);
-        T* dst = j < QCH ? sQ + row * PQ + j * E : sO + row * PO + (j - QCH) * E;
-        *reinterpret_cast<chunk16*>(dst) = stage[i];
-      }
-    }
-    if (tid < BQ) { sL[tid] = st_l; sD[tid] = st_d; }
-  };
-
-  const int qt_begin = P.causal ? (kb * BK) / BQ * BQ : 0;
-  load_tile(qt_begin);
-  for (int qt = qt_begin; qt < S; qt += BQ) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (qt + BQ < S) load_tile(qt + BQ);
-
-    const bool active = k0 < S && (!P.causal || qt + BQ - 1 >= k0);
-    if (!active) continue;
-    const bool need_mask = (P.causal && qt < k0 + 31) || (qt + BQ > S);
-
-    f32x16 sa[BQ / 32], dp[BQ / 32];
-#pragma unroll
-    for (int qb = 0; qb < BQ / 32; ++qb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { sa[qb][r] = 0.f; dp[qb][r] = 0.f; }
-#pragma unroll
-      for (int ks = 0; ks < DQK / 16; ++ks)
-        mma(sa[qb], lds_frag<T>(sQ + (qb * 32 + n) * PQ + ks * 16 + 8 * g), kf[ks]);
-#pragma unroll
-      for (int ks = 0; ks < DV / 16; ++ks)
-        mma(dp[qb], lds_frag<T>(sO + (qb * 32 + n) * PO + ks * 16 + 8 * g), vf[ks]);
-    }
-    // P and dZ (in place): rows = queries qt + qb*32 + (r/4)*8 + g*4 + r%4, column = my key
-#pragma unroll
-    for (int qb = 0; qb < BQ / 32; ++qb)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int qrow = qb * 32 + rr * 8 + g * 4;
-        const f32x4 lq = *reinterpret_cast<const f32x4*>(sL + qrow);
-        const f32x4 dq = *reinterpret_cast<const f32x4*>(sD + qrow);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = rr * 4 + e;
-          float p = fast_exp2(sa[qb][r] * P.scale_log2 - lq[e]);
-          if (need_mask) {
-            const int qi = qt + qrow + e;
-            if (qi >= S || (P.causal && my_k > qi)) p = 0.f;
-          }
-          sa[qb][r] = p;
-          dp[qb][r] = p * (dp[qb][r] - dq[e]);
-        }
-      }
-#pragma unroll
-    for (int kk = 0; kk < BQ / 16; ++kk) {
-      const frag_t<T> pf = acc_to_frag<T>(sa[kk >> 1], kk & 1);
-      const frag_t<T> zf = acc_to_frag<T>(dp[kk >> 1], kk & 1);
-      const int ra = kk * 16 + 4 * g;
-#pragma unroll
-      for (int db = 0; db < DV / 32; ++db) mma(dv[db], TrRead<T>::get(sO, PO, ra, ra + 8, db * 32), pf);
-#pragma unroll
-      for (int db = 0; db < DQK32 / 32; ++db) mma(dk[db], TrRead<T>::get(sQ, PQ, ra, ra + 8, db * 32), zf);
-    }
-  }
-
-  if (my_k >= S) return;
-  const size_t row = (size_t)(b * S + my_k) * H + h;
-  T* dkvr = (T*)P.dkv + row * DKVH;
-  T* dkvl = (T*)P.dkv_lo + row * DKVH;
-  float* dper = P.dkpe_h + row * DR;
-  // dKV as hi (+ lo for bf16): lo = bf16(x - hi) carries the next 8 bits for the GEMMs
-  auto put4 = [&](int col, float a0, float a1, float a2, float a3) {
-    typename FragOf<T>::half hi = {to_elem<T>(a0), to_elem<T>(a1), to_elem<T>(a2), to_elem<T>(a3)};
-    *reinterpret_cast<typename FragOf<T>::half*>(dkvr + col) = hi;
-    if (sizeof(T) == 2) {
-      typename FragOf<T>::half lo = {to_elem<T>(a0 - to_f32(hi[0])), to_elem<T>(a1 - to_f32(hi[1])),
-                                     to_elem<T>(a2 - to_f32(hi[2])), to_elem<T>(a3 - to_f32(hi[3]))};
-      *reinterpret_cast<typename FragOf<T>::half*>(dkvl + col) = lo;
-    }
-  };
-#pragma unroll
-  for (int db = 0; db < DQK32 / 32; ++db)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int d = db * 32 + rr * 8 + g * 4;
-      const float a0 = dk[db][4 * rr] * P.scale, a1 = dk[db][4 * rr + 1] * P.scale;
-      const float a2 = dk[db][4 * rr + 2] * P.scale, a3 = dk[db][4 * rr + 3] * P.scale;
-      if (d < DN) {
-        put4(d, a0, a1, a2, a3);
-      } else if (d < DQK) {
-        f32x4 v = {a0, a1, a2, a3};
-        *reinterpret_cast<f32x4*>(dper + (d - DN)) = v;
-      }
-    }
-#pragma unroll
-  for (int db = 0; db < DV / 32; ++db)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
-      put4(DN + db * 32 + rr * 8 + g * 4, dv[db][4 * rr], dv[db][4 * rr + 1], dv[db][4 * rr + 2], dv[db][4 * rr + 3]);
-}
-
 
 // Key-stationary dK/dV for bf16 with 192/128-wide heads: 32 keys per wave on the
 // 32x32x16 MFMA, one wave per SIMD (4 waves, 128 keys per workgroup). The wave's K and V
@@ -780,9 +581,7 @@ hipError_t launch_attn_bwd(const AttnBwdArgs& a, int stage, hipStream_t st) {
         else dkdv32_kernel<DN, DR, DV, false, false><<<grid, 256, 0, st>>>(P);
       }
     } else {
-      constexpr int BK = 32 * Tl::WPH_KV;
-      P.n_blocks = (a.S + BK - 1) / BK;
-      dkdv_kernel<T, DN, DR, DV, Tl::BQ, Tl::WPH_KV><<<dim3(P.n_blocks * a.H, a.B), 64 * Tl::WPH_KV, 0, st>>>(P);
+      return launch_dkdv_generic<T, DN, DR, DV>(P, a.B, st);
     }
   } else if (stage == 2) {
     return launch_bwd_dq<T, DN, DR, DV>(P, a.B, st);

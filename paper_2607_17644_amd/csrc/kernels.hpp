@@ -103,6 +103,9 @@ struct AttnBwdArgs {
 namespace bwd { struct BwdParams; }
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st);
+// the generic key-stationary dK/dV kernel (attn_bwd_kv.hip)
+template <typename T, int DN, int DR, int DV>
+hipError_t launch_dkdv_generic(bwd::BwdParams P, int B, hipStream_t st);
 
 // stage 0: delta; 1: dK/dV (into dkv, dkpe_h); 2: dQ; 3: dk_pe head sum.
 // (dc_kv / dW are the GEMMs above.)
