@@ -739,12 +739,14 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
 }  // namespace
 
 // dq_ds_kernel's shape: 8 waves (two per SIMD, which hides the latency of the dS^T
-// stream) with one 32-query tile each. Measured at S=16384, H=16: 0.97 ms; 4 waves with
-// two tiles each (one K fragment read feeds two MFMAs) 1.37 ms, 4 waves with one 1.63 ms.
+// stream) with two 32-query tiles each (one K fragment read from LDS feeds two MFMAs,
+// halving the K traffic through LDS), over a three-stage ring (four do not fit in LDS
+// at 46 KB a stage). Measured at S=16384, H=16: 0.96 ms against 1.02 ms for one tile per
+// wave over four stages (bitwise equal); 4 waves with two tiles 1.37 ms, with one 1.63 ms.
 #ifndef DQ_WAVES
 #define DQ_WAVES 8
-#define DQ_TPW 1
-#define DQ_NS 4
+#define DQ_TPW 2
+#define DQ_NS 3
 #endif
 // dq_rec_kernel's shape: 4 waves (one per SIMD, 128 queries per workgroup). Measured at
 // S=16384, H=16: 2.16-2.38 ms; 8 waves need more than their 256 registers (98 spilled):
