@@ -738,16 +738,17 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
 
 }  // namespace
 
-// dq_ds_kernel's shape: 8 waves (two per SIMD, which hides the latency of the dS^T
-// stream) with two 32-query tiles each (one K fragment read from LDS feeds two MFMAs,
-// halving the K traffic through LDS), over a three-stage ring (four do not fit in LDS
-// at 46 KB a stage). Measured at S=16384, H=16: 0.96 ms against 1.02 ms for one tile per
-// wave over four stages (bitwise equal); 4 waves with two tiles 1.37 ms, with one 1.63 ms.
-#ifndef DQ_WAVES
-#define DQ_WAVES 8
-#define DQ_TPW 2
-#define DQ_NS 3
-#endif
+// dq_ds_kernel's shapes: 8 waves (two per SIMD, which hides the latency of the dS^T
+// stream). With two 32-query tiles per wave a K fragment read from LDS feeds two MFMAs,
+// halving the K traffic through LDS, over a three-stage ring (four do not fit in LDS at
+// 46 KB a stage); it needs a grid of at least two workgroups per CU, below which one
+// tile per wave over a four-stage ring (twice the workgroups) is faster. Measured (16
+// heads, dQ stage alone): S=16384 0.98 ms (two tiles) against 1.04 ms (one); S=8192 0.357
+// against 0.278 ms; S=2048 0.084 against 0.050 ms. Both shapes give the same bits. 4 waves
+// with two tiles 1.37 ms, with one 1.63 ms at S=16384.
+constexpr int kDqWaves = 8;
+constexpr long long kDqWideMinGroups = 512;
+
 // dq_rec_kernel's shape: 4 waves (one per SIMD, 128 queries per workgroup). Measured at
 // S=16384, H=16: 2.16-2.38 ms; 8 waves need more than their 256 registers (98 spilled):
 // 7.8 ms. Interleaving one key block's dS arithmetic with the other's MFMAs in a pinned
@@ -771,9 +772,15 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
         P.n_blocks = (P.ds_T + WPH - 1) / WPH;
         dq_ds_fused_kernel<DN, DR, DV><<<dim3(P.n_blocks * P.H, B), 64 * WPH, 0, st>>>(P);
       } else {
-        // DQ_WAVES waves x DQ_TPW query tiles of 32 per workgroup
-        P.n_blocks = (P.ds_T + DQ_WAVES * DQ_TPW - 1) / (DQ_WAVES * DQ_TPW);
-        dq_ds_kernel<DN, DR, DV, DQ_WAVES, DQ_NS, DQ_TPW><<<dim3(P.n_blocks * P.H, B), 64 * DQ_WAVES, 0, st>>>(P);
+        // kDqWaves waves x 1 or 2 query tiles of 32 per workgroup
+        const int nb_wide = (P.ds_T + 2 * kDqWaves - 1) / (2 * kDqWaves);
+        if ((long long)nb_wide * P.H * B >= kDqWideMinGroups) {
+          P.n_blocks = nb_wide;
+          dq_ds_kernel<DN, DR, DV, kDqWaves, 3, 2><<<dim3(P.n_blocks * P.H, B), 64 * kDqWaves, 0, st>>>(P);
+        } else {
+          P.n_blocks = (P.ds_T + kDqWaves - 1) / kDqWaves;
+          dq_ds_kernel<DN, DR, DV, kDqWaves, 4, 1><<<dim3(P.n_blocks * P.H, B), 64 * kDqWaves, 0, st>>>(P);
+        }
       }
       return hipGetLastError();
     }

@@ -149,12 +149,14 @@ def test_head_partition_bitwise(dtype):
     assert scaled_err(acc_dkpe, f64(full["dk_pe"])) < 1e-4
 
 
-def test_workgroup_size_choice_is_invisible():
-    """The forward takes 128 queries per workgroup instead of 256 when the grid would be
-    small: a 32-head run (256) and its 8-head shards (128) agree bit for bit, and so do
-    the gradients computed from them."""
+@pytest.mark.parametrize("S", [4096, 8192])
+def test_workgroup_size_choice_is_invisible(S):
+    """The forward takes 128 queries per workgroup instead of 256, and the dQ pass one
+    query tile per wave instead of two, when the grid would be small: a 32-head run and
+    its 8-head shards (the forward at 256 and 128 queries; at S=8192 also dQ at two and one
+    tiles per wave) agree bit for bit, and so do the gradients computed from them."""
     import torch
-    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=4096, n_heads=32)
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=32)
     x = LI.make_inputs(w)
     d = dev_inputs(w, x)
     full, out, lse = gpu_step(w, d)
