@@ -172,6 +172,25 @@ def test_workgroup_size_choice_is_invisible(S):
         assert torch.equal(g["dw_kv_b"], full["dw_kv_b"][:, r * 2048:(r + 1) * 2048]), r
 
 
+def test_batch_independence_bitwise():
+    """A batch element's outputs do not depend on the other elements of the batch: at
+    S=8192, 16 heads, the 2-element run takes the two-tile dQ shape (512 workgroups) and
+    the 1-element run of its second element the one-tile shape, and out, lse, dq and
+    dk_pe agree bit for bit (dc_kv up to the order of its split sum over heads)."""
+    import torch
+    w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=8192, batch=2)
+    x = LI.make_inputs(w)
+    d = dev_inputs(w, x)
+    g2, out2, lse2 = gpu_step(w, d)
+    w1 = w.replace(batch=1)
+    d1 = {k: (v if k == "w_kv_b" else v[1:2].contiguous()) for k, v in d.items()}
+    g1, out1, lse1 = gpu_step(w1, d1)
+    assert torch.equal(out1, out2[1:2]) and torch.equal(lse1, lse2[1:2])
+    assert torch.equal(g1["dq"], g2["dq"][1:2])
+    assert torch.equal(g1["dk_pe"], g2["dk_pe"][1:2])
+    assert scaled_err(f64(g1["dc_kv"]), f64(g2["dc_kv"][1:2])) < 1e-5
+
+
 def test_repeatable():
     import torch
     w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=700, n_heads=3)
