@@ -243,11 +243,16 @@ __global__ __launch_bounds__(64 * NW, 1) void dq_rec_kernel(BwdParams P) {
   kfill.init(wave, l, H * DKVH);
   vfill.init(wave, l, H * DKVH);
   pfill.init(wave, l, DR);
-  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
+  auto fill_rows = [&](T* dk, T* dp, T* dv, int kt, int rows) {
     const T* kvb = kv + ((size_t)(b * S + kt) * H + h) * DKVH;
-    kfill.fill(dk, wave, l, kvb, H * DKVH, S - kt);
-    vfill.fill(dv, wave, l, kvb + DN, H * DKVH, S - kt);
-    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, S - kt);
+    kfill.fill(dk, wave, l, kvb, H * DKVH, rows);
+    vfill.fill(dv, wave, l, kvb + DN, H * DKVH, rows);
+    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, rows);
+  };
+  // one branch per tile: whole tiles take the copies with no per-instruction row test
+  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
+    if (S - kt >= BC) fill_rows(dk, dp, dv, kt, BC);
+    else fill_rows(dk, dp, dv, kt, S - kt);
   };
 
   constexpr int PF = 3;

@@ -336,14 +336,20 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_ring_kernel(FwdParams P) {
   kfill.init(wave, l, H * DKVH);
   vfill.init(wave, l, H * DKVH);
   pfill.init(wave, l, DR);
-  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
+  auto fill_rows = [&](T* dk, T* dp, T* dv, int kt, int rows) {
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const T* kvb = kv + ((size_t)(b * S + kt) * H + min(h0 + gi, H - 1)) * DKVH;
-      kfill.fill(dk + gi * BC * DN, wave, l, kvb, H * DKVH, S - kt);
-      vfill.fill(dv + gi * BC * DV, wave, l, kvb + DN, H * DKVH, S - kt);
+      kfill.fill(dk + gi * BC * DN, wave, l, kvb, H * DKVH, rows);
+      vfill.fill(dv + gi * BC * DV, wave, l, kvb + DN, H * DKVH, rows);
     }
-    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, S - kt);
+    pfill.fill(dp, wave, l, kpe + (size_t)(b * S + kt) * DR, DR, rows);
+  };
+  // one branch per tile: whole tiles (all but possibly the last) take the copies with no
+  // per-instruction row test
+  auto fill = [&](T* dk, T* dp, T* dv, int kt) {
+    if (S - kt >= BC) fill_rows(dk, dp, dv, kt, BC);
+    else fill_rows(dk, dp, dv, kt, S - kt);
   };
 
   const int ntiles = (kend + BC - 1) / BC;

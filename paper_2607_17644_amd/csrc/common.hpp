@@ -320,14 +320,21 @@ struct SwzRowFill {
     lane_off = rl * stride + ((l % CPR) ^ swz<CPR>(RPI * wave + rl)) * E;
   }
   __device__ __forceinline__ void fill(T* tile, int wave, int l, const T* base, int stride, int rows_valid) const {
-#pragma unroll
-    for (int j = wave; j < NI; j += NW) {
+    auto one = [&](int j) {
       if (rows_valid >= NROWS) {
         g2lds16(base + j * RPI * stride + lane_off, tile + j * 64 * E);
       } else {
         const int row = j * RPI + l / CPR, c = (l % CPR) ^ swz<CPR>(row);
         g2lds16(base + min(row, rows_valid - 1) * stride + c * E, tile + j * 64 * E);
       }
+    };
+    if constexpr (NI % NW == 0) {
+      // the same number of instructions for every wave (wave < NW): no loop branches
+#pragma unroll
+      for (int i = 0; i < NI / NW; ++i) one(wave + i * NW);
+    } else {
+#pragma unroll
+      for (int j = wave; j < NI; j += NW) one(j);
     }
   }
 };
