@@ -72,6 +72,13 @@ def test_v3_fp32_mode_and_latent_width_extremes():
     check(V3.replace(seq_len=65, n_heads=1, d_c=32), gamma=True)
 
 
+@pytest.mark.parametrize("dtype,S,H,B", [("bf16", 300, 4, 2), ("fp32", 65, 3, 1)])
+def test_half_width_heads(dtype, S, H, B):
+    """64/32/64-wide heads (a 32-wide rope band: four 8-element chunks per lane group)."""
+    check(V3.replace(seq_len=S, n_heads=H, batch=B, dtype=dtype, d_c=256, d_nope=64, d_rope=32, d_v=64),
+          gamma=True, offset=11)
+
+
 def test_without_q_and_other_eps_and_base():
     check(V3.replace(seq_len=70, n_heads=2), with_q=False, gamma=True)
     check(TINY.replace(seq_len=50), eps=0.5, base=500.0, gamma=True)
