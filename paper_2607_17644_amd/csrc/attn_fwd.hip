@@ -502,25 +502,33 @@ struct FwdFusedParams {
   int causal;
 };
 
-// Latent rows [kt, kt+nrows) of batch b -> sC (row pitch `pitch` elements): direct
+// Latent rows [kt, kt + NROWS) of batch b -> sC (row pitch `pitch` elements): direct
 // global->LDS loads, one wave instruction per row and 64-chunk segment (lane l lands
-// 16*l bytes after the segment start); rows past S are zero-filled by LDS stores.
-template <typename T>
-__device__ __forceinline__ void load_latent_rows(const T* __restrict__ cg, T* sC, int nrows, int pitch, int nw,
-                                                 int b, int S, int dc, int kt, int wave, int l) {
+// 16*l bytes after the segment start), NROWS / NW rows per wave; rows past S are
+// zero-filled by LDS stores. DCF: d_c at compile time (0: the run-time dc). Whole tiles
+// take the loads with no per-row test.
+template <typename T, int NROWS, int NW, int DCF>
+__device__ __forceinline__ void load_latent_rows(const T* __restrict__ cg, T* sC, int pitch, int b, int S, int dc,
+                                                 int kt, int wave, int l) {
   constexpr int E = Elems16<T>::n;
-  const int row_chunks = dc / E;
-  for (int row = wave; row < nrows; row += nw) {
-    const int key = kt + row;
-    T* dst = sC + row * pitch;
-    for (int seg = 0; seg < row_chunks; seg += 64) {
-      const int c = seg + l;
-      if (c < row_chunks) {
-        if (key < S) g2lds16(cg + ((size_t)(b * S + key) * dc + (size_t)c * E), dst + seg * E);
-        else *reinterpret_cast<chunk16*>(dst + c * E) = zero_chunk();
+  static_assert(NROWS % NW == 0, "whole rows per wave");
+  const int row_chunks = DCF > 0 ? DCF / E : dc / E;
+  auto rows = [&](auto whole) {
+#pragma unroll
+    for (int i = 0; i < NROWS / NW; ++i) {
+      const int row = wave + i * NW, key = kt + row;
+      T* dst = sC + row * pitch;
+      for (int seg = 0; seg < row_chunks; seg += 64) {
+        const int c = seg + l;
+        if (c < row_chunks) {
+          if (decltype(whole)::value || key < S) g2lds16(cg + ((size_t)(b * S + key) * dc + (size_t)c * E), dst + seg * E);
+          else *reinterpret_cast<chunk16*>(dst + c * E) = zero_chunk();
+        }
       }
     }
-  }
+  };
+  if (kt + NROWS <= S) rows(std::true_type{});
+  else rows(std::false_type{});
 }
 
 // DCF: d_c as a compile-time constant (0: the run-time P.d_c, up to DCMAX)
@@ -599,7 +607,7 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
     }
   };
 
-  load_latent_rows<T>(cg, sC, BC, PC, NW, b, S, dc, 0, wave, l);
+  load_latent_rows<T, BC, NW, DCF>(cg, sC, PC, b, S, dc, 0, wave, l);
   load_p(0);
   for (int kt = 0; kt < kend; kt += BC) {
     wait_vmem();                    // this wave's direct loads into sC have landed
@@ -667,7 +675,7 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
     }
     __syncthreads();  // sK / sV / sP complete; sC free
     if (kt + BC < kend) {
-      load_latent_rows<T>(cg, sC, BC, PC, NW, b, S, dc, kt + BC, wave, l);
+      load_latent_rows<T, BC, NW, DCF>(cg, sC, PC, b, S, dc, kt + BC, wave, l);
       load_p(kt + BC);
     }
     fwd_tile<T, DN, DR, DV, BC>(sK, PK, sP, PP, sV, PV, qf, oacc, m, lsum, kt, q0, my_q, S, P.scale_log2,
