@@ -246,6 +246,26 @@ def test_random_shapes():
         check_full(LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal))
 
 
+def test_random_shapes_half_width_heads():
+    """Seeded random (B, S, H, causal, element type, dq mode) at 64/32/64-wide heads with a
+    256-wide latent, fwd + bwd."""
+    rng = np.random.default_rng(2027)
+    for _ in range(6):
+        S = int(rng.integers(1, 700))
+        H = int(rng.integers(1, 6))
+        B = int(rng.integers(1, 3))
+        causal = bool(rng.integers(0, 2))
+        dtype = "bf16" if rng.integers(0, 3) else "fp32"
+        dq_mode = int(rng.integers(0, 2))
+        w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal, dtype=dtype,
+                                                    d_c=256, d_nope=64, d_rope=32, d_v=64)
+        x = LI.make_inputs(w)
+        g, _, _ = gpu_step(w, dev_inputs(w, x), dq_mode=dq_mode)
+        ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+        for k in NAMES:
+            check_tol(k, f64(g[k]), ref[k], w.dtype)
+
+
 def test_s16384_two_heads_against_the_full_oracle():
     """The benchmark's configuration (S=16384, 16 heads) against the full oracle on two of
     its heads: dq and the dW columns of heads 0-1 of the 16-head run (they depend on their
