@@ -352,18 +352,24 @@ def out_proj_bench(w, steps, warmup, sp=8, d_model=7168):
     return res
 
 
-def sweep_bench(w, lengths, steps, warmup):
-    """The default step at shorter gathered sequences (same heads and widths)."""
+def sweep_bench(w, lengths, steps, warmup, graph=False):
+    """The default step at shorter gathered sequences (same heads and widths); with graph,
+    also the step captured once in a HIP graph and replayed (no launch gaps: at short
+    sequences the kernels are a few microseconds each)."""
     import torch
     out = []
     for S in lengths:
         ws = w.replace(seq_len=S)
-        r = StepRunner(ws).time(steps, warmup)
+        runner = StepRunner(ws)
+        r = runner.time(steps, warmup)
         ms = r["ms"]["step"]
         tf = flops(ws) / (ms * 1e-3) / 1e12
+        gms = graph_step_ms(runner.step, steps) if graph else None
         out.append({"seq_len": S, "ms_per_step": round(ms, 4), "tflops": round(tf, 1),
                     "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+                    "graph_ms_per_step": None if gms is None else round(gms, 4),
                     "ms_breakdown": {k: round(v, 4) for k, v in r["ms"].items()}})
+        del runner
         torch.cuda.empty_cache()
     return out
 
@@ -622,7 +628,7 @@ def main():
                          "fwd_out_lse_bitwise_equal_materialised": r["fwd_out_lse_bitwise_equal_materialised"],
                          "grads_bitwise_equal_materialised": r["grads_bitwise_equal_materialised"]}
     if not a.no_extras and a.seq_len is None:
-        line["sweep"] = sweep_bench(w, (2048, 4096, 8192), a.steps, a.warmup)
+        line["sweep"] = sweep_bench(w, (2048, 4096, 8192), a.steps, a.warmup, graph=not a.no_graph)
         progress("S sweep done")
     line["prologue_outside_step"] = g.get("prologue")
     if not a.no_extras and a.seq_len is None and a.heads is None:
