@@ -608,25 +608,31 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
 }
 
 // The same product with the K_nope rebuild organised around its operand traffic (d_c =
-// 512): 4 waves (one per SIMD, 128 queries per workgroup); wave w owns K_nope column
-// block w and keeps its 32 rows of W_h^T (pi-ordered, 32 fragments) in registers for the
-// whole kernel; per 64-key step the latent rows are copied once into LDS (direct loads,
-// one 1 KB row per wave instruction, rows padded to 65 chunks: conflict-free row
-// fragments) and each wave rebuilds its column block for both 32-key halves (two
-// independent accumulator chains), so W_h^T is read once per workgroup and each latent
-// row once per step instead of once per wave and step. Operand roles, contraction
-// order and rounding are those of dq_ds_fused_kernel: the K tile and dq are the same bit
-// for bit.
-template <int DN, int DR, int DV, int DC>
+// 512): 4 waves (one per SIMD); wave w owns K_nope column block w and keeps its 32 rows of
+// W_h^T (pi-ordered, 32 fragments) in registers for the whole kernel, and TPW
+// consecutive 32-query tiles (the rebuilt K tile serves 32 * 4 * TPW queries, which sets
+// the rebuild's share of the work: 1.33x the dQ products at TPW = 2). Per 64-key step the
+// latent rows are copied once into LDS (direct loads, one 1 KB row per wave instruction,
+// rows padded to 65 chunks: conflict-free row fragments) and each wave rebuilds its
+// column block for both 32-key halves (two independent accumulator chains), so W_h^T is
+// read once per workgroup and each latent row once per step. The copies of step s + 1
+// (latent rows into the then free sC, dS^T blocks into the other of two sD stages, k_pe
+// rows into registers) are issued right after the rebuild of step s, so that they land
+// while the step's dQ products run. Operand roles, contraction order and rounding are
+// those of dq_ds_fused_kernel: the K tile and dq are the same bit for bit.
+template <int DN, int DR, int DV, int DC, int TPW>
 __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
   using T = bf16;
   constexpr int DQK = DN + DR, DKVH = DN + DV, NW = 4, KB = 64, NKS = DC / 16;
   constexpr int KP = DQK / 8 + 4;  // K tile pitch in 16-byte chunks (% 8 == 4: transposing reads)
   constexpr int CP = DC / 8 + 1;   // latent row pitch in chunks (odd: row fragments conflict-free)
+  constexpr int DSW = TPW * 2 * 32 * 32;  // dS^T elements per wave and step
   static_assert(DN == NW * 32 && DR == 64 && DC == 64 * 8, "one 32-column K_nope block per wave; a latent row per copy");
+  static_assert(TPW == 1 || TPW == 2, "one or two query tiles per wave");
+  static_assert(KB * DR / 8 == 64 * NW * 2, "two k_pe chunks per thread and step");
   __shared__ __attribute__((aligned(16))) T sC[KB * CP * 8];
   __shared__ __attribute__((aligned(16))) T sK[KB * KP * 8];
-  __shared__ __attribute__((aligned(16))) T sD[NW * 2 * 32 * 32];
+  __shared__ __attribute__((aligned(16))) T sD0[NW * DSW], sD1[NW * DSW];
 
   const T* __restrict__ kpe = (const T*)P.k_pe;
   const T* __restrict__ ds = (const T*)P.ds;
@@ -640,11 +646,16 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
 
   const int tid = threadIdx.x, l = tid & 63, n = l & 31, g = l >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);
-  const int t = qblk * NW + wave;  // this wave's query tile
-  const bool wave_ok = t < TT;
-  const int nk = wave_ok ? ds_tile_keys(TT, P.causal, t) : 0;
-  const T* dtile = ds + (wave_ok ? ds_tile_offset(TT, P.causal, bh, t) : 0);
-  const int kend = P.causal ? min(S, (qblk + 1) * NW * 32) : S;
+  const int t0 = (qblk * NW + wave) * TPW;  // this wave's query tiles t0 .. t0 + TPW - 1
+  int nk[TPW];
+  const T* dtile[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const bool ok = t0 + i < TT;
+    nk[i] = ok ? ds_tile_keys(TT, P.causal, t0 + i) : 0;  // keys stored for the tile
+    dtile[i] = ds + (ok ? ds_tile_offset(TT, P.causal, bh, t0 + i) : 0);
+  }
+  const int kend = P.causal ? min(S, (qblk + 1) * NW * TPW * 32) : S;
   const int nsteps = (kend + KB - 1) / KB;
 
   // W_h^T rows of this wave's column block in the order pi (bits 2 and 3 swapped), so
@@ -658,36 +669,62 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
   }
   const T* cg = (const T*)P.c_kv + (size_t)b * S * DC;
 
-  f32x16 dqa[DQK / 32];
+  f32x16 dqa[TPW][DQK / 32];
 #pragma unroll
-  for (int i = 0; i < DQK / 32; ++i) dqa[i] = f32x16{};
+  for (int i = 0; i < TPW; ++i)
+#pragma unroll
+    for (int j = 0; j < DQK / 32; ++j) dqa[i][j] = f32x16{};
 
-  constexpr int PF = 3;
-  for (int st = 0; st < nsteps; ++st) {
-    const int kt = st * KB;
-    __syncthreads();  // the previous step's reads of sC / sK / sD are done
-    // latent rows kt .. kt + 63 (rows past S clamped: their dS is zero), wave w rows 16 w ..
+  // copies of step s: latent rows kt .. kt + 63 (rows past S clamped: their dS is zero),
+  // wave w rows 16 w ..; the wave's dS^T blocks (a dummy block when not stored); k_pe rows
+  // through registers (stored into the K tile after the next barrier)
+  auto load_latent = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < KB / NW; ++i) {
       const int r = wave * (KB / NW) + i;
       g2lds16(cg + (size_t)min(kt + r, S - 1) * DC + l * 8, sC + r * CP * 8);
     }
+  };
+  auto load_ds = [&](T* sD, int kt) {
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {  // this wave's dS^T blocks of the step (a dummy when not stored)
-      const int kb = kt + 32 * sub;
-      const T* src = kb < nk ? dtile + (size_t)kb * 32 : dtile;
-      g2lds16(src + l * 8, sD + (wave * 2 + sub) * 1024);
-      g2lds16(src + 512 + l * 8, sD + (wave * 2 + sub) * 1024 + 512);
-    }
+    for (int i = 0; i < TPW; ++i)
 #pragma unroll
-    for (int i = 0; i < KB * DR / 8 / (64 * NW); ++i) {  // k_pe rows
+      for (int sub = 0; sub < 2; ++sub) {
+        const int kb = kt + 32 * sub;
+        const T* src = kb < nk[i] ? dtile[i] + (size_t)kb * 32 : dtile[i];
+        T* dst = sD + wave * DSW + (i * 2 + sub) * 1024;
+        g2lds16(src + l * 8, dst);
+        g2lds16(src + 512 + l * 8, dst + 512);
+      }
+  };
+  chunk16 pe[2];
+  auto load_pe = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
       const int c = tid + i * 64 * NW, r = c / (DR / 8), ch = c % (DR / 8);
-      const int key = min(kt + r, S - 1);
-      const chunk16 v = *reinterpret_cast<const chunk16*>(kpe + (size_t)(b * S + key) * DR + ch * 8);
-      *reinterpret_cast<chunk16*>(sK + r * KP * 8 + DN + ch * 8) = v;
+      pe[i] = *reinterpret_cast<const chunk16*>(kpe + (size_t)(b * S + min(kt + r, S - 1)) * DR + ch * 8);
     }
-    wait_vmem();
-    __syncthreads();
+  };
+  auto store_pe = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * 64 * NW, r = c / (DR / 8), ch = c % (DR / 8);
+      *reinterpret_cast<chunk16*>(sK + r * KP * 8 + DN + ch * 8) = pe[i];
+    }
+  };
+
+  constexpr int PF = 3;
+  load_latent(0);
+  load_ds(sD0, 0);
+  load_pe(0);
+  auto step = [&](auto stage, int st) {
+    constexpr int SD = decltype(stage)::value;
+    T* sDc = SD == 0 ? sD0 : sD1;  // this step's dS^T stage
+    T* sDn = SD == 0 ? sD1 : sD0;  // the next step's
+    const int kt = st * KB;
+    wait_vmem();      // this wave's copies of step st (latent rows, dS^T, k_pe) have landed
+    __syncthreads();  // everyone's; the previous step's reads of sK and of sDn are done
+    store_pe();
     {  // K_nope column block `wave` for keys kt .. kt + 63: two chains, one per 32-key half
       auto c_frag = [&](int i) {  // product i: contraction step i / 2 of key half i % 2
         return *reinterpret_cast<const frag_t<T>*>(sC + (32 * (i & 1) + n) * CP * 8 + (i >> 1) * 16 + 8 * g);
@@ -710,35 +747,52 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
         *reinterpret_cast<bf16x8*>(dst + 16) = acc_to_frag<T>(acc[kh], 1);
       }
     }
-    __syncthreads();  // the whole K tile is in LDS
+    __syncthreads();  // the whole K tile is in LDS; every wave's reads of sC are done
+    if (st + 1 < nsteps) {  // the next step's copies, behind this step's dQ products
+      load_latent(kt + KB);
+      load_ds(sDn, kt + KB);
+      load_pe(kt + KB);
+    }
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
-      if (kt + 32 * sub < nk) {  // wave-uniform: key blocks past the tile's queries hold no dS
-        const T* tk = sK + 32 * sub * KP * 8;
-        const T* td = sD + (wave * 2 + sub) * 1024;
+      const T* tk = sK + 32 * sub * KP * 8;
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const int ra = kk * 16 + 4 * g;
-          const bf16x8 zf = pad_tr_frag<4>(td, ra, ra + 8, 0);
+      for (int kk = 0; kk < 2; ++kk) {
+        const int ra = kk * 16 + 4 * g;
+        bf16x8 zf[TPW];
 #pragma unroll
-          for (int db = 0; db < DQK / 32; ++db) mma(dqa[db], pad_tr_frag<KP>(tk, ra, ra + 8, db * 32), zf);
+        for (int i = 0; i < TPW; ++i) zf[i] = pad_tr_frag<4>(sDc + wave * DSW + (i * 2 + sub) * 1024, ra, ra + 8, 0);
+#pragma unroll
+        for (int db = 0; db < DQK / 32; ++db) {
+          const bf16x8 kf = pad_tr_frag<KP>(tk, ra, ra + 8, db * 32);
+          // wave-uniform: key blocks past a tile's queries hold no dS for it
+#pragma unroll
+          for (int i = 0; i < TPW; ++i)
+            if (kt + 32 * sub < nk[i]) mma(dqa[i][db], kf, zf[i]);
         }
       }
     }
+  };
+  for (int st = 0; st < nsteps; st += 2) {
+    step(std::integral_constant<int, 0>{}, st);
+    if (st + 1 < nsteps) step(std::integral_constant<int, 1>{}, st + 1);
   }
 
-  const int my_q = t * 32 + ds_query_of_position(n);
-  if (!wave_ok || my_q >= S) return;
-  T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll
-  for (int db = 0; db < DQK / 32; ++db)
+  for (int i = 0; i < TPW; ++i) {
+    const int my_q = (t0 + i) * 32 + ds_query_of_position(n);
+    if (t0 + i >= TT || my_q >= S) continue;
+    T* dqr = (T*)P.dq + ((size_t)(b * S + my_q) * H + h) * DQK;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      bf16x4 v;
+    for (int db = 0; db < DQK / 32; ++db)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[db][4 * rr + e] * P.scale);
-      *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
-    }
+      for (int rr = 0; rr < 4; ++rr) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = to_elem<T>(dqa[i][db][4 * rr + e] * P.scale);
+        *reinterpret_cast<bf16x4*>(dqr + db * 32 + rr * 8 + g * 4) = v;
+      }
+  }
 }
 
 }  // namespace
@@ -770,8 +824,9 @@ hipError_t launch_bwd_dq(bwd::BwdParams P, int B, hipStream_t st) {
   if constexpr (sizeof(T) == 2 && DN + DR == 192 && DV == 128) {
     if (P.ds) {
       if (P.w_t && P.d_c == kFusedMaxDc) {
-        P.n_blocks = (P.ds_T + 3) / 4;
-        dq_ds_fused2_kernel<DN, DR, DV, kFusedMaxDc><<<dim3(P.n_blocks * P.H, B), 256, 0, st>>>(P);
+        constexpr int TPW = 2;
+        P.n_blocks = (P.ds_T + 4 * TPW - 1) / (4 * TPW);
+        dq_ds_fused2_kernel<DN, DR, DV, kFusedMaxDc, TPW><<<dim3(P.n_blocks * P.H, B), 256, 0, st>>>(P);
       } else if (P.w_t) {
         constexpr int WPH = 8;
         P.n_blocks = (P.ds_T + WPH - 1) / WPH;
