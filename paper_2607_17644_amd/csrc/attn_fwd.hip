@@ -623,22 +623,29 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
         for (int j = 0; j < NKB; ++j)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      // W^T in fragment order: the fragment of column block cb and contraction step ks is
+      // 64 lanes x 8 contiguous elements (one coalesced 1 KB read in bf16)
+      const int nks = dc / 16;
       const T* wrow[NCB];
 #pragma unroll
-      for (int i = 0; i < NCB; ++i) wrow[i] = wt + (size_t)(h * DKVH + (cb0 + i) * 32 + n) * dc + 8 * g;
+      for (int i = 0; i < NCB; ++i) wrow[i] = wt + (size_t)(h * NCBLK + cb0 + i) * nks * 512 + l * 8;
       if constexpr (DCF > 0 && NCB == 1) {
         // d_c known at compile time: the W^T fragments stream from L2 through a ring of
         // WR registers, WR contraction steps ahead of their MFMAs (one load in flight per
         // step would leave every step waiting for L2)
         constexpr int NKS = DCF / 16, WR = 16;
         static_assert(NKS >= WR, "ring shorter than the contraction");
+        // wave-uniform fragment base (scalar registers) + one per-lane offset
+        const T* wsb = wt + (size_t)__builtin_amdgcn_readfirstlane(h * NCBLK + cb0) * NKS * 512;
+        const int loff = l * 8;
+        auto wfrag = [&](int ks) { return *reinterpret_cast<const frag_t<T>*>(wsb + ks * 512 + loff); };
         frag_t<T> ar[WR];
 #pragma unroll
-        for (int u = 0; u < WR; ++u) ar[u] = *reinterpret_cast<const frag_t<T>*>(wrow[0] + u * 16);
+        for (int u = 0; u < WR; ++u) ar[u] = wfrag(u);
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
           const frag_t<T> a = ar[ks % WR];
-          if (ks + WR < NKS) ar[ks % WR] = *reinterpret_cast<const frag_t<T>*>(wrow[0] + (ks + WR) * 16);
+          if (ks + WR < NKS) ar[ks % WR] = wfrag(ks + WR);
           frag_t<T> bb[NKB];
 #pragma unroll
           for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
@@ -649,7 +656,7 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
         for (int ks = 0; ks < dc / 16; ++ks) {
           frag_t<T> a[NCB], bb[NKB];
 #pragma unroll
-          for (int i = 0; i < NCB; ++i) a[i] = *reinterpret_cast<const frag_t<T>*>(wrow[i] + ks * 16);
+          for (int i = 0; i < NCB; ++i) a[i] = *reinterpret_cast<const frag_t<T>*>(wrow[i] + ks * 512);
 #pragma unroll
           for (int j = 0; j < NKB; ++j) bb[j] = lds_frag<T>(sC + (j * 32 + n) * PC + ks * 16 + 8 * g);
 #pragma unroll
@@ -697,6 +704,22 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
       *reinterpret_cast<typename FragOf<T>::half*>(orow + db * 32 + rr * 8 + g * 4) = v;
     }
   if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
+}
+
+// W_kv_b^T in the fused forward's fragment order, one thread per output element: block
+// (cb, ks) of 512 elements holds, for lane l = 32 g + n, the 8 elements
+// w_t[32 cb + n][16 ks + 8 g + e] = w[16 ks + 8 g + e][32 cb + n] (K = d_c rows of w, a
+// multiple of 16; N = H*(DN+DV) columns, a multiple of 32).
+template <typename T>
+__global__ __launch_bounds__(256) void frag_w_kernel(const T* __restrict__ w, T* __restrict__ wf, int K, int N) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * N) return;
+  const int nks = K / 16;
+  const long long blk = i / 512;
+  const int within = (int)(i % 512), lane = within >> 3, e = within & 7;
+  const int cb = (int)(blk / nks), ks = (int)(blk % nks);
+  const int col = cb * 32 + (lane & 31), k = ks * 16 + 8 * (lane >> 5) + e;
+  wf[i] = w[(size_t)k * N + col];
 }
 
 // w_t[n][k] = w[k][n]  (K = d_c rows, N = H*(DN+DV) columns), one thread per output element
@@ -769,7 +792,7 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
   constexpr int BR = 32 * FW;
   const int N = a.H * (DN + DV);
   const long long nw = (long long)a.d_c * N;
-  transpose_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
+  frag_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
   FwdFusedParams P;
   P.q = a.q; P.k_pe = a.k_pe; P.c_kv = a.c_kv; P.w_t = w_t_ws; P.out = a.out; P.lse = a.lse;
   P.S = a.S; P.H = a.H; P.d_c = a.d_c; P.n_qblocks = (a.S + BR - 1) / BR;

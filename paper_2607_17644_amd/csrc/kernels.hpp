@@ -67,8 +67,8 @@ constexpr float kRescaleLog2 = 8.f;
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
 
-// Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T
-// (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
+// Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T in the
+// MFMA fragment order (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
 constexpr int kFusedMaxDc = 512;
 // w_t[n][k] = w[k][n] for w [K, N] (W_kv_b^T for the on-chip K/V rebuilds)
 template <typename T>
