@@ -382,9 +382,10 @@ laga_status_t laga_attn_bwd_stage(int stage, const laga_problem_t* p, const void
 
   const bool on_chip = fused && !kv && kv_on_chip(p);
   if (on_chip) {
-    // the kernels rebuild K/V tiles from c_kv and W_kv_b^T, transposed in the first stage
+    // the kernels rebuild K/V tiles from c_kv and W_kv_b^T, written in fragment order in the
+    // first stage
     if (stage == LAGA_BWD_PREPARE) {
-      hipError_t e = launch_transpose_w<bf16>((const bf16*)w_kv_b, (bf16*)(wsb + ws.w_t), d.d_c, d.H * d.dkvh(), st);
+      hipError_t e = launch_frag_w_pi<bf16>((const bf16*)w_kv_b, (bf16*)(wsb + ws.w_t), d.d_c, d.H * d.dkvh(), st);
       if (e != hipSuccess) return LAGA_ERR_DEVICE;
     }
   } else if (fused && !kv) {

@@ -215,8 +215,10 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
     // the two 16-wide B-operand fragments of that block: no data movement afterwards.
     static_assert(DN % 32 == 0 && DV % 32 == 0, "32-column blocks");
     const int dc = P.d_c;
-    const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
-    const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + pi_n) * dc + 8 * g;
+    // W_h^T in fragment order with each block's rows in the order pi (written so by the
+    // first stage): fragment (column block b, step ks) at wt + (b * dc / 16 + ks) * 512,
+    // one coalesced 1 KB read per wave
+    const T* wt = (const T*)P.w_t + (size_t)h * (DKVH / 32) * (dc / 16) * 512 + l * 8;
     const T* cr = (const T*)P.c_kv + krow * dc + 8 * g;
     constexpr int NB = DKVH / 32;
     f32x16 acc[NB];
@@ -230,7 +232,7 @@ __global__ __launch_bounds__(256, 1) void dkdv32_kernel(BwdParams P) {
         cf[j] = *reinterpret_cast<const frag_t<T>*>(cr + (k0 + j) * 16);
 #pragma unroll
         for (int b = 0; b < NB; ++b)
-          wf[j][b] = *reinterpret_cast<const frag_t<T>*>(wt + (size_t)b * 32 * dc + (k0 + j) * 16);
+          wf[j][b] = *reinterpret_cast<const frag_t<T>*>(wt + ((size_t)b * (dc / 16) + k0 + j) * 512);
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j)

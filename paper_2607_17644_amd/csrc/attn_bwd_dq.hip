@@ -531,10 +531,10 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
   const int nsteps = (kend + KB - 1) / KB;
 
   // this wave's share of the rebuild: key half rk, K_nope column block rb; W^T rows in the
-  // order pi (bits 2 and 3 swapped) so that lane (n, g) holds columns 16 hh + 8 g + e
+  // order pi (bits 2 and 3 swapped) so that lane (n, g) holds columns 16 hh + 8 g + e (the
+  // fragment-ordered copy of W^T holds them so: fragment (block rb, step ks) at wt + ks * 512)
   const int rk = wave >> 2, rb = wave & 3;
-  const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
-  const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + rb * 32 + pi_n) * dc + 8 * g;
+  const T* wt = (const T*)P.w_t + ((size_t)h * (DKVH / 32) + rb) * (dc / 16) * 512 + l * 8;
   const T* cg = (const T*)P.c_kv + (size_t)b * S * dc + 8 * g;
 
   f32x16 dqa[DQK / 32];
@@ -565,7 +565,7 @@ __global__ __launch_bounds__(512, 1) void dq_ds_fused_kernel(BwdParams P) {
         frag_t<T> wa[8], cb[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          wa[j] = *reinterpret_cast<const frag_t<T>*>(wt + (k0 + j) * 16);
+          wa[j] = *reinterpret_cast<const frag_t<T>*>(wt + (k0 + j) * 512);
           cb[j] = *reinterpret_cast<const frag_t<T>*>(cr + (k0 + j) * 16);
         }
 #pragma unroll
@@ -659,13 +659,14 @@ __global__ __launch_bounds__(256, 1) void dq_ds_fused2_kernel(BwdParams P) {
   const int nsteps = (kend + KB - 1) / KB;
 
   // W_h^T rows of this wave's column block in the order pi (bits 2 and 3 swapped), so
-  // that lane (n, g) of the rebuild accumulator holds columns 16 hh + 8 g + e
-  const int pi_n = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
+  // that lane (n, g) of the rebuild accumulator holds columns 16 hh + 8 g + e (the
+  // fragment-ordered copy of W^T holds them so)
   frag_t<T> wf[NKS];
   {
-    const T* wt = (const T*)P.w_t + ((size_t)h * DKVH + wave * 32 + pi_n) * DC + 8 * g;
+    // W_h^T in fragment order: fragment (column block wave, step ks) at wt + ks * 512
+    const T* wt = (const T*)P.w_t + ((size_t)h * (DKVH / 32) + wave) * NKS * 512 + l * 8;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) wf[ks] = *reinterpret_cast<const frag_t<T>*>(wt + ks * 16);
+    for (int ks = 0; ks < NKS; ++ks) wf[ks] = *reinterpret_cast<const frag_t<T>*>(wt + ks * 512);
   }
   const T* cg = (const T*)P.c_kv + (size_t)b * S * DC;
 

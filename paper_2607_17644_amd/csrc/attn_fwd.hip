@@ -706,11 +706,13 @@ __global__ __launch_bounds__(64 * WPH) void attn_fwd_fused_kernel(FwdFusedParams
   if (g == 0) P.lse[(size_t)(b * H + h) * S + my_q] = (m + fast_log2(ltot)) * 0.69314718055994530942f;
 }
 
-// W_kv_b^T in the fused forward's fragment order, one thread per output element: block
-// (cb, ks) of 512 elements holds, for lane l = 32 g + n, the 8 elements
-// w_t[32 cb + n][16 ks + 8 g + e] = w[16 ks + 8 g + e][32 cb + n] (K = d_c rows of w, a
-// multiple of 16; N = H*(DN+DV) columns, a multiple of 32).
-template <typename T>
+// W_kv_b^T in MFMA A-fragment order, one thread per output element: block (cb, ks) of 512
+// elements holds, for lane l = 32 g + n, the 8 elements
+// w_t[32 cb + r(n)][16 ks + 8 g + e] = w[16 ks + 8 g + e][32 cb + r(n)], with r(n) = n, or
+// with PI the order pi (bits 2 and 3 of n swapped) that the backward's rebuilds use (K =
+// d_c rows of w, a multiple of 16; N = H*(DN+DV) columns, a multiple of 32). A wave reads
+// one fragment as 1 KB of contiguous memory.
+template <typename T, bool PI>
 __global__ __launch_bounds__(256) void frag_w_kernel(const T* __restrict__ w, T* __restrict__ wf, int K, int N) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long long)K * N) return;
@@ -718,17 +720,9 @@ __global__ __launch_bounds__(256) void frag_w_kernel(const T* __restrict__ w, T*
   const long long blk = i / 512;
   const int within = (int)(i % 512), lane = within >> 3, e = within & 7;
   const int cb = (int)(blk / nks), ks = (int)(blk % nks);
-  const int col = cb * 32 + (lane & 31), k = ks * 16 + 8 * (lane >> 5) + e;
+  const int n = lane & 31, r = PI ? (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1) : n;
+  const int col = cb * 32 + r, k = ks * 16 + 8 * (lane >> 5) + e;
   wf[i] = w[(size_t)k * N + col];
-}
-
-// w_t[n][k] = w[k][n]  (K = d_c rows, N = H*(DN+DV) columns), one thread per output element
-template <typename T>
-__global__ __launch_bounds__(256) void transpose_w_kernel(const T* __restrict__ w, T* __restrict__ w_t, int K, int N) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * N) return;
-  const int n = (int)(i / K), k = (int)(i % K);
-  w_t[i] = w[(size_t)k * N + n];
 }
 
 template <typename T, int DN, int DR, int DV> struct FwdTiles;
@@ -792,7 +786,7 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
   constexpr int BR = 32 * FW;
   const int N = a.H * (DN + DV);
   const long long nw = (long long)a.d_c * N;
-  frag_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
+  frag_w_kernel<T, false><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>((const T*)a.w, (T*)w_t_ws, a.d_c, N);
   FwdFusedParams P;
   P.q = a.q; P.k_pe = a.k_pe; P.c_kv = a.c_kv; P.w_t = w_t_ws; P.out = a.out; P.lse = a.lse;
   P.S = a.S; P.H = a.H; P.d_c = a.d_c; P.n_qblocks = (a.S + BR - 1) / BR;
@@ -807,13 +801,12 @@ hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t
 }
 
 template <typename T>
-hipError_t launch_transpose_w(const T* w, T* w_t, int K, int N, hipStream_t st) {
+hipError_t launch_frag_w_pi(const T* w, T* w_t, int K, int N, hipStream_t st) {
   const long long nw = (long long)K * N;
-  transpose_w_kernel<T><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>(w, w_t, K, N);
+  frag_w_kernel<T, true><<<(unsigned)((nw + 255) / 256), 256, 0, st>>>(w, w_t, K, N);
   return hipGetLastError();
 }
-template hipError_t launch_transpose_w<bf16>(const bf16*, bf16*, int, int, hipStream_t);
-template hipError_t launch_transpose_w<float>(const float*, float*, int, int, hipStream_t);
+template hipError_t launch_frag_w_pi<bf16>(const bf16*, bf16*, int, int, hipStream_t);
 
 #define LAGA_INST_FWD(T, DN, DR, DV)                                                      \
   template hipError_t launch_attn_fwd<T, DN, DR, DV>(const AttnFwdArgs&, hipStream_t);    \

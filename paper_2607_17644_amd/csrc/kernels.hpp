@@ -70,9 +70,13 @@ hipError_t launch_attn_fwd(const AttnFwdArgs& a, hipStream_t st);
 // Fused forward: K/V rebuilt tile by tile from c_kv; w_t_ws receives W_kv_b^T in the
 // MFMA fragment order (H*(DN+DV) x d_c elements) first. d_c <= kFusedMaxDc.
 constexpr int kFusedMaxDc = 512;
-// w_t[n][k] = w[k][n] for w [K, N] (W_kv_b^T for the on-chip K/V rebuilds)
+// W_kv_b^T (w [K = d_c, N]) in MFMA A-fragment order with the rows of each 32-row block
+// in the order pi (bits 2 and 3 swapped), for the backward's on-chip K/V rebuilds: the
+// fragment of row block cb and contraction step ks is the 512 elements at
+// (cb * (K / 16) + ks) * 512, lane l = 32 g + n holding row 32 cb + pi(n), elements
+// 16 ks + 8 g .. + 7.
 template <typename T>
-hipError_t launch_transpose_w(const T* w, T* w_t, int K, int N, hipStream_t st);
+hipError_t launch_frag_w_pi(const T* w, T* w_t, int K, int N, hipStream_t st);
 template <typename T, int DN, int DR, int DV>
 hipError_t launch_attn_fwd_fused(const AttnFwdArgs& a, void* w_t_ws, hipStream_t st);
 
