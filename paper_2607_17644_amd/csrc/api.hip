@@ -38,10 +38,12 @@ laga_status_t validate(const laga_problem_t* p, Dims* d) {
   if (p->kv_mode != LAGA_KV_MATERIALIZED && p->kv_mode != LAGA_KV_FUSED) return LAGA_ERR_UNSUPPORTED;
   if (!is_v3(p) && !is_small(p) && !is_half(p)) return LAGA_ERR_UNSUPPORTED;
   if (p->d_c % 32 != 0 || p->d_c > 1024) return LAGA_ERR_UNSUPPORTED;
+  // each factor below 2^31 before any product is formed, so no product overflows int64
+  if (p->batch >= kMaxElems || p->seq_len >= kMaxElems || p->n_heads >= kMaxElems) return LAGA_ERR_UNSUPPORTED;
   const int64_t tok = p->batch * p->seq_len;
   const int64_t wide = p->n_heads * (p->d_nope + (p->d_rope > p->d_v ? p->d_rope : p->d_v) +
                                      (p->d_nope > p->d_v ? p->d_nope : p->d_v));
-  if (tok >= kMaxElems || tok * wide >= kMaxElems || tok * p->d_c >= kMaxElems ||
+  if (tok >= kMaxElems || wide >= kMaxElems || tok * wide >= kMaxElems || tok * p->d_c >= kMaxElems ||
       p->d_c * p->n_heads * (p->d_nope + p->d_v) * 16 >= kMaxElems)
     return LAGA_ERR_UNSUPPORTED;
   d->B = (int)p->batch; d->S = (int)p->seq_len; d->H = (int)p->n_heads; d->d_c = (int)p->d_c;
@@ -135,6 +137,9 @@ laga_status_t validate_out_proj(const laga_out_proj_t* p, OutDims* d) {
   if (!p) return LAGA_ERR_NULL;
   if (p->tokens <= 0 || p->n_heads <= 0 || p->d_v <= 0 || p->d_model <= 0) return LAGA_ERR_SHAPE;
   if (p->reserved != 0 || (p->dtype != LAGA_DTYPE_BF16 && p->dtype != LAGA_DTYPE_FP32)) return LAGA_ERR_UNSUPPORTED;
+  // each factor below 2^31 before any product is formed, so no product overflows int64
+  if (p->tokens >= kMaxElems || p->n_heads >= kMaxElems || p->d_v >= kMaxElems || p->d_model >= kMaxElems)
+    return LAGA_ERR_UNSUPPORTED;
   const int64_t F = p->n_heads * p->d_v;
   if (F % 16 != 0 || p->d_model % 16 != 0) return LAGA_ERR_UNSUPPORTED;
   if (F >= kMaxElems || p->tokens * F >= kMaxElems || p->tokens * p->d_model >= kMaxElems ||

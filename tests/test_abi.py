@@ -67,6 +67,11 @@ def test_validation_errors_without_launch():
         Q = B.Problem(**{**P.__dict__, "seq_len": S, "n_heads": H})
         assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == code, (S, H)
         assert lib.laga_workspace_bytes(ctypes.byref(Q.c()), 1) == 0
+    # factors whose product would overflow 64 bits are rejected, not multiplied
+    for field, val in (("batch", 1 << 40), ("seq_len", 1 << 40), ("n_heads", 1 << 40), ("n_heads", 1 << 31)):
+        Q = B.Problem(**{**P.__dict__, field: val, **({"batch": 1 << 40} if field == "seq_len" else {})})
+        assert lib.laga_reconstruct_kv(ctypes.byref(Q.c()), fake, fake, fake, None) == 3, (field, val)
+        assert lib.laga_workspace_bytes(ctypes.byref(Q.c()), 1) == 0
     Q = B.Problem(**{**P.__dict__, "seq_len": s_max, "n_heads": 16})
     assert lib.laga_workspace_bytes(ctypes.byref(Q.c()), 1) > 0  # the largest accepted size
     # misaligned
@@ -157,3 +162,22 @@ def test_workspace_sizes_follow_the_header():
     # fp32 stores no dS^T (4.3 GB in bf16 at S=16384, 16 heads): its workspace is linear in S
     P = B.Problem(1, 16384, 16, 512, 128, 64, 128, 0.072, dtype=B.DTYPE_FP32)
     assert lib.laga_workspace_bytes(ctypes.byref(P.c()), 1) < 1 << 30
+
+
+def test_out_proj_entry_points_validate_first():
+    """laga_out_proj_*: the size checks of include/laga.h, before any pointer is used."""
+    lib, B = _raw()
+    fake = ctypes.c_void_p(0x10000)
+    ok = B.OutProj(64, 4, 32, 64)
+    assert lib.laga_out_proj_workspace_bytes(ctypes.byref(B.OutProj(4096, 16, 128, 7168).c())) > 0
+    assert lib.laga_out_proj_fwd(None, fake, fake, fake, None) == 1
+    assert lib.laga_out_proj_fwd(ctypes.byref(ok.c()), None, fake, fake, None) == 1
+    assert lib.laga_out_proj_fwd(ctypes.byref(ok.c()), ctypes.c_void_p(0x10008), fake, fake, None) == 4
+    bad = {2: [dict(tokens=0), dict(n_heads=-1), dict(d_model=0)],
+           3: [dict(d_v=7), dict(d_model=40), dict(dtype=9), dict(reserved=1), dict(tokens=1 << 31),
+               dict(tokens=1 << 40, d_model=1 << 40), dict(n_heads=1 << 40), dict(tokens=1 << 20, d_model=1 << 12)]}
+    for code, cases in bad.items():
+        for kw in cases:
+            Q = B.OutProj(**{**ok.__dict__, **kw})
+            assert lib.laga_out_proj_fwd(ctypes.byref(Q.c()), fake, fake, fake, None) == code, kw
+            assert lib.laga_out_proj_workspace_bytes(ctypes.byref(Q.c())) == 0, kw
