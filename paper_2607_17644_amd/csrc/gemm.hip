@@ -14,7 +14,8 @@
 //
 // The reconstruct (a 512-long contraction writing 256 bytes per output row and head)
 // runs as a persistent variant of the large-tile kernel that spreads each tile's
-// stores over the next tile's MFMAs (gemm_stream_kernel).
+// stores over the next tile's MFMAs (gemm_stream_kernel); dc and dW, whose dKV operand
+// comes as a bf16 pair hi + lo, run the large tiles on eight waves (gemm_big8_kernel).
 //
 // Per output element the contraction runs over K in ascending 16-wide steps
 // (one MFMA each) with fp32 accumulation; tile shapes and the dW token split do
@@ -215,7 +216,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
 // one wave per SIMD, each wave 128 x 128 (4 x 4 blocks of 32 x 32, 256 accumulator
 // registers per lane): an LDS operand fragment then feeds four MFMAs, so LDS reads
 // stay well under the LDS rate. Besides 256 x 256, 128 x 512 and 512 x 128 tiles cover
-// a whole 512-wide side, so the other (large) operand is read from memory once.
+// a whole 512-wide side, so the other (large) operand is read from memory once (the
+// backward's dc and dW take those shapes on gemm_big8_kernel below, two waves per SIMD).
 // The contraction advances 32 at a time through an LDS ring of NSLOT stages filled by
 // direct global->LDS copies issued NSLOT - 1 stages ahead (a stage of MFMAs is shorter
 // than the latency of a load from memory); one barrier per stage, placed inside the
@@ -236,16 +238,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
 constexpr int kGK = 32;  // contraction per stage
 
 // This lane's share of the copies of one operand tile (ROWS / 16 instructions, wave w
-// issues w, w + 4, ...).
-template <bool KS, int ROWS>
+// of NWV issues w, w + NWV, ...).
+template <bool KS, int ROWS, int NWV = 4>
 struct GFill {
-  static constexpr int NI = ROWS / 16, PER = NI / 4, CPR = ROWS / 8;
+  static constexpr int NI = ROWS / 16, PER = NI / NWV, CPR = ROWS / 8;
+  static_assert(PER * NWV == NI, "whole copy instructions per wave");
   uint32_t off[PER];  // byte offsets from the stage origin of the operand
   // r0: first row (column for KS) of the tile; rlim: number of rows (columns) in the operand.
   __device__ __forceinline__ void init(int wave, int l, int ld, int r0, int rlim) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int p = (wave + 4 * i) * 64 + l;
+      const int p = (wave + NWV * i) * 64 + l;
       if (!KS) {
         const int row = p >> 2, c = (p & 3) ^ ((row >> 2) & 3);
         off[i] = 2u * (uint32_t)(min(r0 + row, rlim - 1) * ld + c * 8);  // rows past the end read the last
@@ -257,15 +260,16 @@ struct GFill {
   }
   __device__ __forceinline__ void fill(const bf16* stage_origin, bf16* tile, int wave) const {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) g2lds16_so(stage_origin, off[i], tile + (wave + 4 * i) * 512);
+    for (int i = 0; i < PER; ++i) g2lds16_so(stage_origin, off[i], tile + (wave + NWV * i) * 512);
   }
 };
 
-// Operand fragments of one wave's four 32-row blocks (rows 128 wsel .. +127 of the
-// tile), contraction step ks (16 wide) of the stage.
-template <bool KS, int ROWS>
+// Operand fragments of one wave's BW 32-row blocks (rows 32 BW wsel .. of the tile),
+// contraction step ks (16 wide) of the stage.
+template <bool KS, int ROWS, int BW = 4>
 struct GRead {
-  int off[4];  // element offsets: k-contiguous uses [0..1] (per ks), k-strided [0..3] (per block)
+  static_assert(BW == 2 || BW == 4, "two or four blocks per wave");
+  int off[BW > 2 ? BW : 2];  // element offsets: k-contiguous uses [0..1] (per ks), k-strided one per block
   __device__ __forceinline__ void init(int l, int wsel) {
     const int g = l >> 5;
     if (!KS) {
@@ -273,15 +277,16 @@ struct GRead {
       for (int ks = 0; ks < 2; ++ks) off[ks] = (l & 31) * kGK + ((2 * ks + g) ^ ((l >> 2) & 3)) * 8;
     } else {
       // transposing read of k rows ra + s/4 (ra = 16 ks + 8 g; second half ra + 4) and
-      // columns 32 b + 16 ((l >> 4) & 1) + 4 (s & 3) .. +3, s = l % 16, b = 4 wsel + j
+      // columns 32 b + 16 ((l >> 4) & 1) + 4 (s & 3) .. +3, s = l % 16, b = BW wsel + j;
+      // logical chunk 4 b + lc of k row r sits at chunk 4 (b ^ (r & 3)) + lc, r & 3 = s / 4
       const int s = l & 15, j4 = s >> 2, lc = 2 * ((l >> 4) & 1) + ((s & 3) >> 1);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        off[j] = j4 * ROWS + 8 * g * ROWS + (4 * (4 * wsel + (j ^ j4)) + lc) * 8 + 4 * (s & 1);
+      for (int j = 0; j < BW; ++j)
+        off[j] = j4 * ROWS + 8 * g * ROWS + (4 * ((BW * wsel + j) ^ j4) + lc) * 8 + 4 * (s & 1);
     }
   }
   __device__ __forceinline__ bf16x8 get(const bf16* tile, int wsel, int ks, int j) const {
-    if (!KS) return *reinterpret_cast<const bf16x8*>(tile + (128 * wsel + 32 * j) * kGK + off[ks]);
+    if (!KS) return *reinterpret_cast<const bf16x8*>(tile + (32 * BW * wsel + 32 * j) * kGK + off[ks]);
     typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
     const bf16* p = tile + off[j] + 16 * ks * ROWS;
     const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
@@ -438,6 +443,138 @@ __global__ __launch_bounds__(256, 1) void gemm_big_kernel(
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int n = n0 + 128 * wn + 32 * j + rr * 8 + g * 4;
+        if (n < N)
+          store4<TO>(Cz + (size_t)m * ldc + n, acc[j][i][4 * rr], acc[j][i][4 * rr + 1], acc[j][i][4 * rr + 2],
+                     acc[j][i][4 * rr + 3]);
+      }
+    }
+}
+
+// The same product on eight waves, two per SIMD, for the contractions with a low-half
+// operand (the backward's dc and dW): each wave owns 64 x 128 (BM <= BN) or 128 x 64 of
+// the output, 8 accumulator blocks (128 registers), so two waves fit on a SIMD and one
+// wave's copies, LDS reads and barrier waits overlap the other's MFMAs. Stages, copies,
+// swizzles and the per-element accumulation order (ascending 16-wide steps, hi before
+// lo per step) are gemm_big_kernel's, so results are bit-identical to it.
+template <int BM, int BN, bool A_KS, bool B_KS, int SPLIT, typename TO>
+__global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ B, const bf16* __restrict__ X2, TO* __restrict__ C,
+    int M, int N, int K, int lda, int ldb, int ldc, int k_chunk, long long split_stride) {
+  static_assert(BM * BN == 4 * 128 * 128 && SPLIT >= 1, "the 4-wave tile shapes, with a low-half operand");
+  constexpr int NWV = 8;
+  constexpr int WGM = BM <= BN ? 2 : 4, WGN = NWV / WGM;  // waves along m, along n
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;           // one wave's output tile
+  constexpr int NI = WTM / 32, NJ = WTN / 32;             // its 32 x 32 blocks
+  static_assert(NI * NJ == 8 && (NI == 2 || NI == 4) && (NJ == 2 || NJ == 4), "8 blocks per wave");
+  constexpr int NT = 3, NSLOT = 3;                        // operand tiles per stage; ring depth (144 KB)
+  constexpr bool X_KS = SPLIT == 1 ? A_KS : B_KS;
+  constexpr int XR = SPLIT == 1 ? BM : BN;
+  constexpr int XB = SPLIT == 1 ? NI : NJ;                // X2 blocks per wave
+  constexpr int TA = BM * kGK, TB = BN * kGK, TX = XR * kGK;
+  constexpr int STAGE = TA + TB + TX;
+  (void)NT;
+  __shared__ __attribute__((aligned(16))) bf16 sm[NSLOT * STAGE];
+
+  const int n_tiles = (N + BN - 1) / BN, m_tiles = (M + BM - 1) / BM;
+  const int lin = xcd_remap(blockIdx.x, n_tiles * m_tiles);
+  const int tn = lin % n_tiles, tm = lin / n_tiles;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kb = blockIdx.z * k_chunk;
+  const int nst = (min(K, kb + k_chunk) - kb) / kGK;
+
+  const int l = threadIdx.x & 63, g = l >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & (NWV - 1);
+  const int wm = wave % WGM, wn = wave / WGM;
+
+  GFill<A_KS, BM, NWV> fa;
+  GFill<B_KS, BN, NWV> fb;
+  GFill<X_KS, XR, NWV> fx;
+  fa.init(wave, l, lda, m0, M);
+  fb.init(wave, l, ldb, n0, N);
+  fx.init(wave, l, SPLIT == 1 ? lda : ldb, SPLIT == 1 ? m0 : n0, SPLIT == 1 ? M : N);
+  auto fill = [&](int slot, int k) {
+    bf16* st = sm + slot * STAGE;
+    fa.fill(A_KS ? A + (size_t)k * lda : A + k, st, wave);
+    fb.fill(B_KS ? B + (size_t)k * ldb : B + k, st + TA, wave);
+    if (SPLIT == 1) fx.fill(A_KS ? X2 + (size_t)k * lda : X2 + k, st + TA + TB, wave);
+    if (SPLIT == 2) fx.fill(B_KS ? X2 + (size_t)k * ldb : X2 + k, st + TA + TB, wave);
+  };
+  constexpr int F = GFill<A_KS, BM, NWV>::PER + GFill<B_KS, BN, NWV>::PER + GFill<X_KS, XR, NWV>::PER;
+  auto wait_stage = [](int ahead) {
+    if (ahead >= 2) wait_vmem_le<2 * F>();
+    else if (ahead == 1) wait_vmem_le<F>();
+    else wait_vmem();
+  };
+  static_assert(2 * F < 64, "vmcnt range");
+
+  GRead<A_KS, BM, NI> ra;
+  GRead<B_KS, BN, NJ> rb;
+  GRead<X_KS, XR, XB> rx;
+  ra.init(l, wm);
+  rb.init(l, wn);
+  const int xsel = SPLIT == 1 ? wm : wn;
+  rx.init(l, xsel);
+
+  f32x16 acc[NJ][NI];  // [n block][m block]: C^T blocks, lane <-> m, 4 consecutive n per lane
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int i = 0; i < NI; ++i) acc[j][i] = f32x16{};
+
+  bf16x8 fA[2][NI], fB[2][NJ], fX[2][XB];
+  auto read = [&](int slot, int ks) {
+    const bf16* st = sm + slot * STAGE;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) fA[ks][i] = ra.get(st, wm, ks, i);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) fB[ks][j] = rb.get(st + TA, wn, ks, j);
+#pragma unroll
+    for (int x = 0; x < XB; ++x) fX[ks][x] = rx.get(st + TA + TB, xsel, ks, x);
+  };
+  // every hi product of the step, then every lo one (per accumulator: hi before lo)
+  auto mmas = [&](int ks) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) mma(acc[j][i], fB[ks][j], fA[ks][i]);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
+        if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
+      }
+  };
+
+  const int npre = min(NSLOT, nst);
+  for (int t = 0; t < npre; ++t) fill(t, kb + t * kGK);
+  wait_stage(npre - 1);
+  lds_barrier();
+  read(0, 0);
+  for (int t = 0; t < nst - 1; ++t) {
+    const int slot = t % NSLOT;
+    read(slot, 1);
+    mmas(0);
+    wait_stage(min(NSLOT - 2, nst - 2 - t));  // this wave's copies of stage t + 1 have landed
+    lds_barrier();                            // ... everyone's; every read of stage t is done
+    if (t + NSLOT < nst) fill(slot, kb + (t + NSLOT) * kGK);
+    read((t + 1) % NSLOT, 0);
+    mmas(1);
+  }
+  read((nst - 1) % NSLOT, 1);
+  mmas(0);
+  mmas(1);
+
+  TO* Cz = C + blockIdx.z * split_stride;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int m = m0 + WTM * wm + 32 * i + (l & 31);
+      if (m >= M) continue;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int n = n0 + WTN * wn + 32 * j + rr * 8 + g * 4;
         if (n < N)
           store4<TO>(Cz + (size_t)m * ldc + n, acc[j][i][4 * rr], acc[j][i][4 * rr + 1], acc[j][i][4 * rr + 2],
                      acc[j][i][4 * rr + 3]);
@@ -756,7 +893,7 @@ hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, float
   if constexpr (sizeof(T) == 2) {
     if (dkv_lo && gemm_big_ok(M, N, K, k_chunk, (size_t)M * K, (size_t)N * K)) {
       if (dc_bm(N) == 128)
-        gemm_big_kernel<128, 512, false, false, 1, float><<<dim3(grid_tiles(M, N, 128, 512), 1, nz), 256, 0, st>>>(
+        gemm_big8_kernel<128, 512, false, false, 1, float><<<dim3(grid_tiles(M, N, 128, 512), 1, nz), 512, 0, st>>>(
             dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
       else
         gemm_big_kernel<256, 256, false, false, 1, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 256, 0, st>>>(
@@ -790,7 +927,7 @@ hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float
   if constexpr (sizeof(T) == 2) {
     if (dkv_lo && gemm_big_ok(M, N, K, split, (size_t)K * M, (size_t)K * N)) {
       if (M > 256)
-        gemm_big_kernel<512, 128, true, true, 2, float><<<dim3(grid_tiles(M, N, 512, 128), 1, nsplit), 256, 0, st>>>(
+        gemm_big8_kernel<512, 128, true, true, 2, float><<<dim3(grid_tiles(M, N, 512, 128), 1, nsplit), 512, 0, st>>>(
             c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
       else
         gemm_big_kernel<256, 256, true, true, 2, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nsplit), 256, 0, st>>>(
