@@ -450,29 +450,29 @@ __global__ __launch_bounds__(256, 1) void gemm_big_kernel(
     }
 }
 
-// The same product on eight waves, two per SIMD, for the contractions with a low-half
-// operand (the backward's dc and dW): each wave owns 64 x 128 (BM <= BN) or 128 x 64 of
-// the output, 8 accumulator blocks (128 registers), so two waves fit on a SIMD and one
-// wave's copies, LDS reads and barrier waits overlap the other's MFMAs. Stages, copies,
-// swizzles and the per-element accumulation order (ascending 16-wide steps, hi before
-// lo per step) are gemm_big_kernel's, so results are bit-identical to it.
+// The same product on eight waves, two per SIMD (the backward's dc and dW, whose dKV
+// operand is a bf16 pair hi + lo, and W_o's backward): each wave owns 64 x 128
+// (BM <= BN) or 128 x 64 of the output, 8 accumulator blocks (128 registers), so two
+// waves fit on a SIMD and one wave's copies, LDS reads and barrier waits overlap the
+// other's MFMAs. Stages, copies, swizzles and the per-element accumulation order
+// (ascending 16-wide steps, hi before lo per step) are gemm_big_kernel's, so results
+// are bit-identical to it.
 template <int BM, int BN, bool A_KS, bool B_KS, int SPLIT, typename TO>
 __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ B, const bf16* __restrict__ X2, TO* __restrict__ C,
     int M, int N, int K, int lda, int ldb, int ldc, int k_chunk, long long split_stride) {
-  static_assert(BM * BN == 4 * 128 * 128 && SPLIT >= 1, "the 4-wave tile shapes, with a low-half operand");
+  static_assert(BM * BN == 4 * 128 * 128, "the 4-wave tile shapes");
   constexpr int NWV = 8;
   constexpr int WGM = BM <= BN ? 2 : 4, WGN = NWV / WGM;  // waves along m, along n
   constexpr int WTM = BM / WGM, WTN = BN / WGN;           // one wave's output tile
   constexpr int NI = WTM / 32, NJ = WTN / 32;             // its 32 x 32 blocks
   static_assert(NI * NJ == 8 && (NI == 2 || NI == 4) && (NJ == 2 || NJ == 4), "8 blocks per wave");
-  constexpr int NT = 3, NSLOT = 3;                        // operand tiles per stage; ring depth (144 KB)
+  constexpr int NSLOT = SPLIT ? 3 : 4;                    // ring depth (144 or 128 KB)
   constexpr bool X_KS = SPLIT == 1 ? A_KS : B_KS;
   constexpr int XR = SPLIT == 1 ? BM : BN;
   constexpr int XB = SPLIT == 1 ? NI : NJ;                // X2 blocks per wave
-  constexpr int TA = BM * kGK, TB = BN * kGK, TX = XR * kGK;
+  constexpr int TA = BM * kGK, TB = BN * kGK, TX = SPLIT ? XR * kGK : 0;
   constexpr int STAGE = TA + TB + TX;
-  (void)NT;
   __shared__ __attribute__((aligned(16))) bf16 sm[NSLOT * STAGE];
 
   const int n_tiles = (N + BN - 1) / BN, m_tiles = (M + BM - 1) / BM;
@@ -491,7 +491,7 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
   GFill<X_KS, XR, NWV> fx;
   fa.init(wave, l, lda, m0, M);
   fb.init(wave, l, ldb, n0, N);
-  fx.init(wave, l, SPLIT == 1 ? lda : ldb, SPLIT == 1 ? m0 : n0, SPLIT == 1 ? M : N);
+  if (SPLIT) fx.init(wave, l, SPLIT == 1 ? lda : ldb, SPLIT == 1 ? m0 : n0, SPLIT == 1 ? M : N);
   auto fill = [&](int slot, int k) {
     bf16* st = sm + slot * STAGE;
     fa.fill(A_KS ? A + (size_t)k * lda : A + k, st, wave);
@@ -499,13 +499,14 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
     if (SPLIT == 1) fx.fill(A_KS ? X2 + (size_t)k * lda : X2 + k, st + TA + TB, wave);
     if (SPLIT == 2) fx.fill(B_KS ? X2 + (size_t)k * ldb : X2 + k, st + TA + TB, wave);
   };
-  constexpr int F = GFill<A_KS, BM, NWV>::PER + GFill<B_KS, BN, NWV>::PER + GFill<X_KS, XR, NWV>::PER;
+  constexpr int F = GFill<A_KS, BM, NWV>::PER + GFill<B_KS, BN, NWV>::PER + (SPLIT ? GFill<X_KS, XR, NWV>::PER : 0);
   auto wait_stage = [](int ahead) {
-    if (ahead >= 2) wait_vmem_le<2 * F>();
+    if (ahead >= 3) wait_vmem_le<3 * F>();
+    else if (ahead == 2) wait_vmem_le<2 * F>();
     else if (ahead == 1) wait_vmem_le<F>();
     else wait_vmem();
   };
-  static_assert(2 * F < 64, "vmcnt range");
+  static_assert(3 * F < 64, "vmcnt range");
 
   GRead<A_KS, BM, NI> ra;
   GRead<B_KS, BN, NJ> rb;
@@ -513,7 +514,7 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
   ra.init(l, wm);
   rb.init(l, wn);
   const int xsel = SPLIT == 1 ? wm : wn;
-  rx.init(l, xsel);
+  if (SPLIT) rx.init(l, xsel);
 
   f32x16 acc[NJ][NI];  // [n block][m block]: C^T blocks, lane <-> m, 4 consecutive n per lane
 #pragma unroll
@@ -528,8 +529,9 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
     for (int i = 0; i < NI; ++i) fA[ks][i] = ra.get(st, wm, ks, i);
 #pragma unroll
     for (int j = 0; j < NJ; ++j) fB[ks][j] = rb.get(st + TA, wn, ks, j);
+    if (SPLIT)
 #pragma unroll
-    for (int x = 0; x < XB; ++x) fX[ks][x] = rx.get(st + TA + TB, xsel, ks, x);
+      for (int x = 0; x < XB; ++x) fX[ks][x] = rx.get(st + TA + TB, xsel, ks, x);
   };
   // every hi product of the step, then every lo one (per accumulator: hi before lo)
   auto mmas = [&](int ks) {
@@ -537,13 +539,14 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int i = 0; i < NI; ++i) mma(acc[j][i], fB[ks][j], fA[ks][i]);
+    if (SPLIT)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
-        if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
-      }
+        for (int i = 0; i < NI; ++i) {
+          if (SPLIT == 1) mma(acc[j][i], fB[ks][j], fX[ks][i]);
+          if (SPLIT == 2) mma(acc[j][i], fX[ks][j], fA[ks][i]);
+        }
   };
 
   const int npre = min(NSLOT, nst);
@@ -896,7 +899,7 @@ hipError_t launch_dc(const T* dkv, const T* dkv_lo, const T* w, float* dc, float
         gemm_big8_kernel<128, 512, false, false, 1, float><<<dim3(grid_tiles(M, N, 128, 512), 1, nz), 512, 0, st>>>(
             dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
       else
-        gemm_big_kernel<256, 256, false, false, 1, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 256, 0, st>>>(
+        gemm_big8_kernel<256, 256, false, false, 1, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 512, 0, st>>>(
             dkv, w, dkv_lo, target, M, N, K, K, K, N, k_chunk, (long long)M * N);
       grid.x = 0;  // done
     }
@@ -930,7 +933,7 @@ hipError_t launch_dw(const T* c, const T* dkv, const T* dkv_lo, float* dw, float
         gemm_big8_kernel<512, 128, true, true, 2, float><<<dim3(grid_tiles(M, N, 512, 128), 1, nsplit), 512, 0, st>>>(
             c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
       else
-        gemm_big_kernel<256, 256, true, true, 2, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nsplit), 256, 0, st>>>(
+        gemm_big8_kernel<256, 256, true, true, 2, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nsplit), 512, 0, st>>>(
             c, dkv, dkv_lo, target, M, N, K, M, N, N, split, (long long)M * N);
       grid.x = 0;  // done
     }
@@ -955,7 +958,7 @@ hipError_t launch_gemm_nt(const T* a, const T* w, T* c, int M, int N, int K, hip
   using G = GemmCfg<T>;
   if constexpr (sizeof(T) == 2) {
     if (gemm_big_ok(M, N, K, K, (size_t)M * K, (size_t)N * K)) {
-      gemm_big_kernel<256, 256, false, false, 0, bf16><<<grid_tiles(M, N, 256, 256), 256, 0, st>>>(
+      gemm_big8_kernel<256, 256, false, false, 0, bf16><<<grid_tiles(M, N, 256, 256), 512, 0, st>>>(
           a, w, nullptr, c, M, N, K, K, K, N, K, 0);
       return hipGetLastError();
     }
@@ -986,7 +989,7 @@ hipError_t launch_gemm_tn(const T* a, const T* b, float* c, float* partial, int 
   bool done = false;
   if constexpr (sizeof(T) == 2) {
     if (gemm_big_ok(M, N, K, split, (size_t)K * M, (size_t)K * N)) {
-      gemm_big_kernel<256, 256, true, true, 0, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 256, 0, st>>>(
+      gemm_big8_kernel<256, 256, true, true, 0, float><<<dim3(grid_tiles(M, N, 256, 256), 1, nz), 512, 0, st>>>(
           a, b, nullptr, target, M, N, K, M, N, N, split, (long long)M * N);
       done = true;
     }
