@@ -353,3 +353,41 @@ def test_s16384_sixteen_heads_against_the_full_oracle():
           " ".join(f"{k} {v[0]:.2e} (rms-scaled {v[1]:.2e})" for k, v in errs.items()))
     for k in NAMES:
         check_tol(k, f64(g[k]), ref[k], "bf16")
+
+
+def test_random_widths_latents_and_modes():
+    """Seeded random problems over every supported head width, latent widths 128-512 and
+    both dq modes: the full backward against the oracle, and the fused-K/V mode (forward
+    and backward) bit for bit equal to the materialised one."""
+    import torch
+    import paper_2607_17644_amd as L
+    widths = {"v3": (128, 64, 128), "half": (64, 32, 64), "small": (32, 16, 32)}
+    rng = np.random.default_rng(2029)
+    for case in range(10):
+        name = ("v3", "v3", "half", "small")[int(rng.integers(0, 4))]
+        dn, dr, dv = widths[name]
+        d_c = (512, 256, 128)[int(rng.integers(0, 3))] if name == "v3" else 512
+        S, H, B = int(rng.integers(1, 1500)), int(rng.integers(1, 7)), int(rng.integers(1, 3))
+        causal, dq_mode = bool(rng.integers(0, 4) > 0), int(rng.integers(0, 2))
+        w = LI.WORKLOADS["v3_train_s16384"].replace(seq_len=S, n_heads=H, batch=B, causal=causal, d_c=d_c,
+                                                     d_nope=dn, d_rope=dr, d_v=dv, seed=300 + case)
+        where = (name, d_c, S, H, B, causal, dq_mode)
+        x = LI.make_inputs(w)
+        d = dev_inputs(w, x)
+        p = problem_for(w, dq_mode=dq_mode)
+        kv = L.laga_reconstruct_kv(p, d["c_kv"], d["w_kv_b"])
+        out, lse = L.laga_attn_fwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv=kv)
+        g = L.laga_attn_bwd(p, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], kv, out, lse, d["dout"])
+        pf = problem_for(w, dq_mode=dq_mode, kv_mode=L.KV_FUSED)
+        of, lf = L.laga_attn_fwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"])
+        gf = L.laga_attn_bwd(pf, d["q"], d["c_kv"], d["k_pe"], d["w_kv_b"], None, of, lf, d["dout"])
+        torch.cuda.synchronize()
+        assert torch.equal(of, out) and torch.equal(lf, lse), where
+        for n, a, b in zip(NAMES, g, gf):
+            assert torch.equal(a, b), (n,) + where
+        ref = O.attn_bwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], x["dout"], **okw(w))
+        ro, rl = O.attn_fwd(x["q"], x["c_kv"], x["k_pe"], x["w_kv_b"], **okw(w))
+        check_tol("out", f64(out), ro, "bf16", where)
+        check_tol("lse", f64(lse), rl, "bf16", where)
+        for n, a in zip(NAMES, g):
+            check_tol(n, f64(a), ref[n], "bf16", where)
