@@ -586,18 +586,18 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
 }
 
 // ------------------------------------------------------------------ streamed large tiles (bf16 out)
-// The 4-wave 256 x 256 tile of gemm_big_kernel (no split, bf16 output) for a short
-// contraction such as the latent's 512, where the 256 x 256 x 2-byte results of a tile
-// take as long to write as its MFMAs take to compute, and a workgroup per tile writes
-// them all at once while every other CU does the same. Here a persistent workgroup
-// takes tiles q = blockIdx.x, + gridDim.x, ... and one LDS ring runs through all of
-// them (the next tile's first stages are copied while the current one finishes). A
-// finished tile's accumulators are rounded to bf16 and paired across the two
-// half-waves (v_permlane32_swap: 8 consecutive columns per lane) into 32 16-byte
-// stores per wave, and those stores are issued two per stage over the first 16 stages
-// of the next tile, so the writes run at an even rate behind the MFMAs. Per output
-// element the products are accumulated in the same order as in gemm_big_kernel: the
-// results are bitwise equal.
+// The 256 x 256 tile (no split, bf16 output) for a short contraction such as the
+// latent's 512, where the 256 x 256 x 2-byte results of a tile take as long to write as
+// its MFMAs take to compute, and a workgroup per tile writes them all at once while
+// every other CU does the same. Here a persistent workgroup takes tiles q = blockIdx.x,
+// + gridDim.x, ... and one LDS ring runs through all of them (the next tile's first
+// stages are copied while the current one finishes). Eight waves, two per SIMD, each
+// own 128 x 64 of the tile (8 accumulator blocks). A finished tile's accumulators are
+// rounded to bf16 and paired across the two half-waves (v_permlane32_swap: 8
+// consecutive columns per lane) into 16 16-byte stores per wave, issued one per stage
+// over the 16 stages of the next tile, so the writes run at an even rate behind the
+// MFMAs. Per output element the products are accumulated in the same order as in
+// gemm_big_kernel: the results are bitwise equal.
 //
 // Stores and copies share the in-order vmcnt counter: the stores issued in the last
 // three stages are younger than the copies a stage waits for (those were issued three
@@ -605,12 +605,13 @@ __global__ __launch_bounds__(512, 1) void gemm_big8_kernel(
 // many more operations in flight.
 constexpr int kStreamStoreStages = 16;  // stages over which a tile's stores are spread
 
+
 template <int BM, int BN, bool A_KS, bool B_KS>
-__global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restrict__ A, const bf16* __restrict__ B,
+__global__ __launch_bounds__(512, 1) void gemm_stream_kernel(const bf16* __restrict__ A, const bf16* __restrict__ B,
                                                              bf16* __restrict__ C, int M, int N, int K, int lda,
                                                              int ldb, int ldc) {
-  static_assert(BM * BN == 4 * 128 * 128 && BM % 128 == 0 && BN % 128 == 0, "four 128 x 128 waves");
-  constexpr int WM = BM / 128;
+  static_assert(BM == 256 && BN == 256, "eight 128 x 64 waves");
+  constexpr int WM = 2;  // waves along m (128 rows each); four along n (64 columns each)
   constexpr int NSLOT = 4;
   constexpr int TA = BM * kGK, TB = BN * kGK, STAGE = TA + TB;
   __shared__ __attribute__((aligned(16))) bf16 sm[NSLOT * STAGE];
@@ -622,11 +623,11 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
   const int total = mine * nst;                              // stages of this workgroup
 
   const int l = threadIdx.x & 63, g = l >> 5;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 7;
   const int wm = wave % WM, wn = wave / WM;
 
-  GFill<A_KS, BM> fa;
-  GFill<B_KS, BN> fb;
+  GFill<A_KS, BM, 8> fa;
+  GFill<B_KS, BN, 8> fb;
   fa.init(wave, l, lda, 0, BM);  // offsets within a tile; the tile origin goes into the base
   fb.init(wave, l, ldb, 0, BN);
   auto tile_at = [&](int it, int& m0, int& n0) {
@@ -651,25 +652,24 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
       }
     }
   };
-  constexpr int F = GFill<A_KS, BM>::PER + GFill<B_KS, BN>::PER;  // copies per wave and stage
-  constexpr int Y = 6;  // stores younger than the copies a stage waits for, in steady state
+  constexpr int F = GFill<A_KS, BM, 8>::PER + GFill<B_KS, BN, 8>::PER;  // copies per wave and stage
+  constexpr int Y = 3;  // stores younger than the copies a stage waits for, in steady state
   static_assert(3 * F + Y + 2 < 64, "vmcnt range");
 
-  GRead<A_KS, BM> ra;
-  GRead<B_KS, BN> rb;
+  GRead<A_KS, BM, 4> ra;
+  GRead<B_KS, BN, 2> rb;
   ra.init(l, wm);
   rb.init(l, wn);
 
-  f32x16 acc[4][4];
-  bf16x8 fA[2][4], fB[2][4];
-  u32x4 pay[16][2];  // the previous tile's results, block (j, i) = 4 j + i, as stored
+  f32x16 acc[2][4];
+  bf16x8 fA[2][4], fB[2][2];
+  u32x4 pay[8][2];  // the previous tile's results, block (j, i) = 4 j + i, as stored
   auto read = [&](int slot, int ks) {
     const bf16* st = sm + slot * STAGE;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      fA[ks][j] = ra.get(st, wm, ks, j);
-      fB[ks][j] = rb.get(st + TA, wn, ks, j);
-    }
+    for (int i = 0; i < 4; ++i) fA[ks][i] = ra.get(st, wm, ks, i);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) fB[ks][j] = rb.get(st + TA, wn, ks, j);
   };
   auto mmas = [&](int ks, int j0, int j1) {
 #pragma unroll
@@ -696,14 +696,14 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
       out[p] = u32x4{r[0], s[0], r[1], s[1]};
     }
   };
-  auto store = [&](const u32x4 (&v)[2], int m0, int n0, int b) {
+  // half hh (columns 16 hh .. of the block) of block b: one 16-byte store per lane
+  auto store = [&](const u32x4 (&v)[2], int m0, int n0, int b, int hh) {
     const int j = b >> 2, i = b & 3;
-    bf16* row = C + (size_t)(m0 + 128 * wm + 32 * i + (l & 31)) * ldc + n0 + 128 * wn + 32 * j + 8 * g;
-    *reinterpret_cast<u32x4*>(row) = v[0];
-    *reinterpret_cast<u32x4*>(row + 16) = v[1];
+    bf16* row = C + (size_t)(m0 + 128 * wm + 32 * i + (l & 31)) * ldc + n0 + 64 * wn + 32 * j + 8 * g;
+    *reinterpret_cast<u32x4*>(row + 16 * hh) = v[hh];
   };
 
-  constexpr int RPS = (A_KS ? 8 : 4) + (B_KS ? 8 : 4);  // LDS reads per step
+  constexpr int RPS = (A_KS ? 8 : 4) + (B_KS ? 4 : 2);  // LDS reads per step
   constexpr int DS_READ = 0x100, MFMA = 0x008;
   // First half of stage t: step-1 reads interleaved with the step-0 MFMAs (which
   // restart every accumulator from zero in the first stage of a tile), then half of
@@ -712,22 +712,22 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
     read(t % NSLOT, 1);
     if (first) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           acc[j][i] = f32x16{};
           mma(acc[j][i], fB[0][j], fA[0][i]);
         }
     } else {
-      mmas(0, 0, 4);
+      mmas(0, 0, 2);
     }
-    mmas(1, 0, 2);
+    mmas(1, 0, 1);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 4, 0);
-      __builtin_amdgcn_sched_group_barrier(MFMA, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(MFMA, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(MFMA, 4, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
   // Second half of stage t: wait for stage t + 1, barrier, refill the slot of stage t,
@@ -745,11 +745,11 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
     fill_next(t % NSLOT);
     __builtin_amdgcn_sched_barrier(0);
     read((t + 1) % NSLOT, 0);  // (after the last stage: a harmless read of a stale slot)
-    mmas(1, 2, 4);
+    mmas(1, 1, 2);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       __builtin_amdgcn_sched_group_barrier(DS_READ, RPS / 2, 0);
-      __builtin_amdgcn_sched_group_barrier(MFMA, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(MFMA, 2, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -767,7 +767,7 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
 #pragma unroll
     for (int s = 0; s < kStreamStoreStages; ++s, ++t) {
       head(t, s == 0);
-      if (it > 0) store(pay[s], e_m0, e_n0, s);
+      if (it > 0) store(pay[s >> 1], e_m0, e_n0, s >> 1, s & 1);
       tail(t, exact);
     }
   };
@@ -782,12 +782,15 @@ __global__ __launch_bounds__(256, 1) void gemm_stream_kernel(const bf16* __restr
       tail(t, std::false_type{});
     }
 #pragma unroll
-    for (int b = 0; b < 16; ++b) pack(b >> 2, b & 3, pay[b]);
+    for (int b = 0; b < 8; ++b) pack(b >> 2, b & 3, pay[b]);
     e_m0 = c_m0;
     e_n0 = c_n0;
   }
 #pragma unroll
-  for (int b = 0; b < 16; ++b) store(pay[b], e_m0, e_n0, b);
+  for (int b = 0; b < 8; ++b) {
+    store(pay[b], e_m0, e_n0, b, 0);
+    store(pay[b], e_m0, e_n0, b, 1);
+  }
   wait_vmem();  // the surplus copies land before the workgroup's LDS is released
 }
 
@@ -833,7 +836,7 @@ hipError_t launch_reconstruct(const T* c, const T* w, T* kv, int M, int N, int K
   if constexpr (sizeof(T) == 2) {
     if (gemm_stream_ok(M, N, K, (size_t)M * K, (size_t)K * N)) {
       const int tiles = grid_tiles(M, N, 256, 256);
-      gemm_stream_kernel<256, 256, false, true><<<tiles < kCUs ? tiles : kCUs, 256, 0, st>>>(
+      gemm_stream_kernel<256, 256, false, true><<<tiles < kCUs ? tiles : kCUs, 512, 0, st>>>(
           c, w, kv, M, N, K, /*lda=*/K, /*ldb=*/N, /*ldc=*/N);
       return hipGetLastError();
     }
